@@ -1,0 +1,243 @@
+"""Pins of the oracle's packed linear (CPU only).
+
+The paper prints no worked GEMV example, so the oracle is pinned to things
+the mathematics fixes: exact rational arithmetic computed from the trits (not
+from the codes), closed-form special cases of eq. 3, and invariants.  Each
+pin is a function of a GEMV callable, and ``test_pins_catch_planted_mistakes``
+checks that plausible mistakes planted into a copy of the oracle (a dropped
+offset, a flipped sign, a shifted group index, a transposed operand, ...)
+each fail at least one pin.
+"""
+
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import codec, packed
+from paper_2609_09240_amd import synth
+
+
+def _pack(inp):
+    c0, b0 = codec.pack(inp.t0.reshape(-1, 128))
+    c1, b1 = codec.pack(inp.t1.reshape(-1, 128)) if inp.nnz1 else (np.zeros(0, np.uint8), 0)
+    assert b0 == 0 and b1 == 0
+    return c0, c1
+
+
+def _args(inp):
+    c0, c1 = _pack(inp)
+    return (inp.n_out, inp.n_in, c0, inp.s0, inp.rowptr1, inp.gidx1, c1, inp.mu1, inp.s1)
+
+
+def oracle_gemv(inp, x):
+    return packed.gemv(*_args(inp), x)
+
+
+def exact_gemv(inp, x):
+    """y in exact rationals, straight from eq. 3 on the trits."""
+    ng = inp.n_in // 128
+    rec = {}
+    for r in range(inp.n_out):
+        for k in range(int(inp.rowptr1[r]), int(inp.rowptr1[r + 1])):
+            rec[(r, int(inp.gidx1[k]))] = k
+    xf = [Fraction(float(v)) for v in x]
+    y = []
+    for r in range(inp.n_out):
+        acc = Fraction(0)
+        for g in range(ng):
+            s0 = Fraction(float(inp.s0[r, g]))
+            k = rec.get((r, g))
+            for i in range(128):
+                w = s0 * int(inp.t0[r, 128 * g + i])
+                if k is not None:
+                    w += Fraction(float(inp.mu1[k])) + Fraction(float(inp.s1[k])) * int(inp.t1[k, i])
+                acc += w * xf[128 * g + i]
+        y.append(acc)
+    return y
+
+
+def tiny(n_out, n_in, f2, seed):
+    inp = synth.linear(n_out, n_in, f2, (seed, 9, 0, 0))
+    x = synth.activations(n_in, (seed, 9, 0, 0))
+    return inp, x
+
+
+# ---------------------------------------------------------------- pins
+
+def pin_exact_rationals(gemv_fn):
+    for (n, k, f2, seed) in [(3, 128, 0.0, 1), (4, 256, 0.5, 2), (8, 512, 0.25, 3), (5, 384, 1.0, 4)]:
+        inp, x = tiny(n, k, f2, seed)
+        y = gemv_fn(inp, x)
+        ex = exact_gemv(inp, x)
+        mag = np.abs(packed.dequantize(*_args(inp)[:9])) @ np.abs(x.astype(np.float64))
+        for r in range(n):
+            if abs(float(ex[r]) - y[r]) > 1e-12 * max(mag[r], 1e-30):
+                return False
+    return True
+
+
+def pin_unit_vectors(gemv_fn):
+    """x = e_k returns column k of W^, built from the trits by hand."""
+    inp, _ = tiny(6, 384, 0.4, 5)
+    assert inp.nnz1 > 0
+    rows = np.repeat(np.arange(6), np.diff(inp.rowptr1))
+    # probe a column inside a two-plane group and one inside a one-plane group
+    r0, g0 = int(rows[0]), int(inp.gidx1[0])
+    cols = [128 * g0 + 17, 128 * g0 + 127, 5]
+    for col in cols:
+        x = np.zeros(384, np.float16)
+        x[col] = 1.0
+        y = gemv_fn(inp, x)
+        g = col // 128
+        for r in range(6):
+            w = float(inp.s0[r, g]) * int(inp.t0[r, col])
+            for k in range(int(inp.rowptr1[r]), int(inp.rowptr1[r + 1])):
+                if int(inp.gidx1[k]) == g:
+                    w += float(inp.mu1[k]) + float(inp.s1[k]) * int(inp.t1[k, col % 128])
+            if y[r] != w:
+                return False
+    return True
+
+
+def pin_all_plus_one(gemv_fn):
+    """T0 = +1 everywhere, one plane, x = 1:  y_r = 128 * sum_g s0[r, g]."""
+    inp, _ = tiny(4, 512, 0.0, 6)
+    inp.t0[:] = 1
+    y = gemv_fn(inp, np.ones(512, np.float16))
+    want = 128.0 * inp.s0.astype(np.float64).sum(axis=1)
+    return np.allclose(y, want, rtol=1e-14, atol=0)
+
+
+def pin_zero_planes(gemv_fn):
+    """T0 = 0 and no second plane: y is exactly +0."""
+    inp, x = tiny(4, 256, 0.0, 7)
+    inp.t0[:] = 0
+    y = gemv_fn(inp, x)
+    return np.all(y == 0)
+
+
+def pin_offset_only(gemv_fn):
+    """T0 = T1 = 0 on two-plane groups: y_r = sum over records of mu * sum(x_g)."""
+    inp, x = tiny(5, 512, 0.5, 8)
+    inp.t0[:] = 0
+    inp.t1[:] = 0
+    y = gemv_fn(inp, x)
+    xs = x.astype(np.float64).reshape(-1, 128).sum(axis=1)
+    want = np.zeros(5)
+    for r in range(5):
+        for k in range(int(inp.rowptr1[r]), int(inp.rowptr1[r + 1])):
+            want[r] += float(inp.mu1[k]) * xs[int(inp.gidx1[k])]
+    return np.allclose(y, want, rtol=1e-12, atol=1e-15)
+
+
+def pin_negation(gemv_fn):
+    """Negating every support and offset negates y (eq. 3 is linear in them)."""
+    inp, x = tiny(6, 256, 0.5, 9)
+    y = gemv_fn(inp, x)
+    inp.t0 *= -1
+    inp.t1 *= -1
+    inp.mu1 = -inp.mu1
+    return np.allclose(gemv_fn(inp, x), -y, rtol=1e-14, atol=1e-15)
+
+
+PINS = [pin_exact_rationals, pin_unit_vectors, pin_all_plus_one, pin_zero_planes,
+        pin_offset_only, pin_negation]
+
+
+@pytest.mark.parametrize("pin", PINS, ids=lambda p: p.__name__)
+def test_oracle_gemv_pins(pin):
+    assert pin(oracle_gemv)
+
+
+# --------------------------------------------------- planted mistakes (oracle copies)
+
+def _mutant(kind):
+    def gemv_fn(inp, x):
+        n, k, c0, s0, rp, gi, c1, mu, s1 = _args(inp)
+        if kind == "drop_offset":
+            mu = np.zeros_like(mu)
+        elif kind == "drop_plane1":
+            s1 = np.zeros_like(s1)
+        elif kind == "flip_plane1_sign":
+            s1 = -s1
+        elif kind == "shift_group":
+            ng = k // 128
+            gi = ((gi.astype(np.int64) + 1) % ng).astype(np.uint16)
+        elif kind == "reverse_digits":
+            g = codec.from_storage(c0, n * k // 128).astype(np.int64)
+            d = (g[..., None] // codec.POW3) % 3
+            g = (d[..., ::-1] * codec.POW3).sum(-1)
+            c0 = codec.to_storage(g.astype(np.uint8))
+        elif kind == "transpose":
+            w = packed.dequantize(n, k, c0, s0, rp, gi, c1, mu, s1)
+            if n == k:
+                return w.T @ x.astype(np.float64)
+            return w @ x.astype(np.float64)[::-1]
+        elif kind == "scale_per_row":
+            s0 = np.repeat(s0[:, :1], s0.shape[1], axis=1)
+        return packed.gemv(n, k, c0, s0, rp, gi, c1, mu, s1, x)
+    return gemv_fn
+
+
+@pytest.mark.parametrize("kind", ["drop_offset", "drop_plane1", "flip_plane1_sign", "shift_group",
+                                  "reverse_digits", "transpose", "scale_per_row"])
+def test_pins_catch_planted_mistakes(kind):
+    mutant = _mutant(kind)
+    assert not all(pin(mutant) for pin in PINS), kind
+
+
+# ------------------------------------------------------------- other pins
+
+def test_dense_matmul_equality_on_tiny_shapes():
+    """Group form == dense W built entry by entry from the trits (fp64, exact)."""
+    inp, x = tiny(7, 384, 0.3, 11)
+    w = np.zeros((7, 384))
+    for r in range(7):
+        for c in range(384):
+            w[r, c] = float(inp.s0[r, c // 128]) * int(inp.t0[r, c])
+        for k in range(int(inp.rowptr1[r]), int(inp.rowptr1[r + 1])):
+            g = int(inp.gidx1[k])
+            for i in range(128):
+                w[r, 128 * g + i] += float(inp.mu1[k]) + float(inp.s1[k]) * int(inp.t1[k, i])
+    np.testing.assert_array_equal(packed.dequantize(*_args(inp)), w)
+    np.testing.assert_allclose(oracle_gemv(inp, x), w @ x.astype(np.float64), rtol=1e-13, atol=1e-13)
+
+
+def test_gemm_rows_equal_gemv():
+    inp, _ = tiny(9, 256, 0.3, 12)
+    X = synth.activations(256, (12, 9, 0, 1), batch=5, outlier_frac=0.01)
+    Y = packed.gemm(*_args(inp), X)
+    for b in range(5):
+        np.testing.assert_allclose(Y[b], oracle_gemv(inp, X[b]), rtol=1e-13, atol=1e-14)
+
+
+def test_dequantize_fp16_closed_forms():
+    inp, _ = tiny(16, 512, 0.2, 13)
+    args = _args(inp)
+    w16 = packed.dequantize_fp16(*args)
+    w64 = packed.dequantize(*args)
+    two = np.zeros((16, 4), bool)
+    rows = np.repeat(np.arange(16), np.diff(inp.rowptr1))
+    two[rows, inp.gidx1.astype(int)] = True
+    two_cols = np.repeat(two, 128, axis=1)
+    # one-plane weights are exactly +s0, -s0 or +0 (positive zero)
+    s0 = np.repeat(inp.s0, 128, axis=1)
+    t0 = inp.t0
+    one = ~two_cols
+    want = np.where(t0 > 0, s0, np.where(t0 < 0, -s0, np.float16(0)))
+    assert np.array_equal(w16[one].view(np.uint16), want[one].view(np.uint16))
+    # two-plane weights lie within one fp16 ulp of the exact fp64 value
+    exact = w64[two_cols]
+    got = w16[two_cols].astype(np.float64)
+    ulp = np.spacing(np.abs(exact).astype(np.float16)).astype(np.float64)
+    assert np.all(np.abs(got - exact) <= ulp)
+
+
+def test_error_bound_dominates_weighted_l1():
+    inp, x = tiny(6, 512, 0.5, 14)
+    args = _args(inp)
+    w = packed.dequantize(*args)
+    b = packed.error_bound(inp.n_out, inp.n_in, inp.s0, inp.rowptr1, inp.gidx1, inp.mu1, inp.s1, x)
+    l1 = np.abs(w) @ np.abs(x.astype(np.float64))
+    assert np.all(b >= 2e-3 * l1 * (1 - 1e-12))
