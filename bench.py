@@ -1,0 +1,231 @@
+"""Benchmark: the Qwen3-8B decode-step linear stack as packed ternary GEMVs.
+
+One step = every packed linear of one decode step at batch 1: 36 layers x
+{q, k, v, o, gate, up, down} (252 matrices, 6.95 G weights), run in
+dependency order as 144 launches per step (q+k+v grouped, o, gate+up grouped,
+down), captured once in a HIP graph and replayed.  Inputs are seeded
+synthetic stand-ins for the paper's converted weights (shapes of section 3,
+10% two-plane groups) and stay resident in HBM; the 1.70 GB of packed weights
+is far larger than the caches, so every step streams them from HBM.
+
+Prints one JSON line: value = aggregate GB/s of algorithmic bytes (packed
+weights + activations + outputs) per step time, plus ms_per_step, the
+roofline of the GEMV kernel (per-launch durations from HIP events on the
+launch stream) and the CPU oracle timed on a bounded sample.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--layers 36]
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def build_stack(layers, device):
+    """Generate (host threads) and pack (GPU) every projection of the stack."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import torch
+
+    from paper_2609_09240_amd import synth, tq
+    names = [n for n, _, _ in synth.PROJECTIONS]
+    mats, xs = [], []
+    t0 = time.time()
+    gen = lambda layer: [synth.projection(n, layer, cfg=3) for n in names]  # noqa: E731
+    with ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
+        pending = [ex.submit(gen, layer) for layer in range(min(layers, 8))]
+        for layer in range(layers):
+            inputs = pending[layer].result()
+            pending[layer] = None
+            if layer + 8 < layers:
+                pending.append(ex.submit(gen, layer + 8))
+            mats.append({n: tq.PackedLinear.from_inputs(inp, device) for n, inp in zip(names, inputs)})
+            xs.append([torch.from_numpy(synth.stage_activations(s, layer, cfg=3)).to(device)
+                       for s in range(len(synth.STAGES))])
+            if layer % 6 == 5 or layer == layers - 1:
+                torch.cuda.synchronize()
+                log(f"built layers 0..{layer} ({time.time() - t0:.1f} s)")
+    return mats, xs
+
+
+def step_launches(mats, xs):
+    """The launches of one decode step, in dependency order."""
+    from paper_2609_09240_amd import synth
+    out = []
+    for layer in range(len(mats)):
+        for s, names in enumerate(synth.STAGES):
+            out.append(([mats[layer][n] for n in names], xs[layer][s]))
+    return out
+
+
+def algorithmic_bytes(launches):
+    total = 0
+    for ms, x in launches:
+        for m in ms:
+            total += m.nbytes() + 2 * m.n_in + 2 * m.n_out
+    return total
+
+
+def cpu_baseline(layers=2):
+    """The oracle (numpy fp64) on the first `layers` layers of the same stack."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import accounting, codec, packed
+    from paper_2609_09240_amd import synth
+    nbytes, secs = 0, 0.0
+    for layer in range(layers):
+        for name, _, _ in synth.PROJECTIONS:
+            inp = synth.projection(name, layer, cfg=3)
+            x = synth.stage_activations(synth.STAGE_OF[name], layer, cfg=3)
+            c0, _ = codec.pack(inp.t0.reshape(-1, 128))
+            c1, _ = codec.pack(inp.t1.reshape(-1, 128))
+            t = time.perf_counter()
+            y = packed.gemv(inp.n_out, inp.n_in, c0, inp.s0, inp.rowptr1, inp.gidx1, c1, inp.mu1, inp.s1, x)
+            secs += time.perf_counter() - t
+            assert np.all(np.isfinite(y))
+            nbytes += accounting.gemv_bytes(inp.n_out, inp.n_in, inp.nnz1)
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return {"value": round(nbytes / secs / 1e9, 6), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"oracle gemv (decode + fp64 dequant + fp64 matvec) of layers 0..{layers - 1} "
+                      f"(7 projections each, {nbytes} algorithmic bytes) in {secs:.1f} s; "
+                      f"host has {os.cpu_count()} logical CPUs"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--layers", type=int, default=36)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the packed GEMV path is single-device; "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_09240_amd import tq
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    tq.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    mats, xs = build_stack(args.layers, dev)
+    launches = step_launches(mats, xs)
+    step_bytes = algorithmic_bytes(launches)
+    weight_bytes = sum(m.nbytes() for ms, _ in launches for m in ms)
+    n_weights = sum(m.n_out * m.n_in for ms, _ in launches for m in ms)
+    outs = [[torch.empty(m.n_out, dtype=torch.float16, device=dev) for m in ms] for ms, _ in launches]
+
+    stream = torch.cuda.Stream()
+
+    def run_step():
+        for (ms, x), ys in zip(launches, outs):
+            if len(ms) == 1:
+                tq.tq_gemv(ms[0], x, y=ys[0], stream=stream)
+            else:
+                tq.tq_gemv_grouped(ms, x, ys=ys, stream=stream)
+
+    with torch.cuda.stream(stream):
+        run_step()                                  # first launches outside capture
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        run_step()
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_stop = torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        t_start.record(stream)
+        for _ in range(args.steps):
+            graph.replay()
+        t_stop.record(stream)
+    torch.cuda.synchronize()
+    ms_total = t_start.elapsed_time(t_stop)
+    ms_per_step = ms_total / args.steps
+    gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
+    log(f"{args.steps} steps: {ms_per_step * 1e3:.1f} us/step, {gbs:.1f} GB/s")
+
+    # Roofline of the GEMV kernel: HIP events around each launch on its stream.
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in launches]
+    durations = []
+    for rep in range(2):
+        with torch.cuda.stream(stream):
+            for (ms, x), ys, (a, b) in zip(launches, outs, ev):
+                a.record(stream)
+                if len(ms) == 1:
+                    tq.tq_gemv(ms[0], x, y=ys[0], stream=stream)
+                else:
+                    tq.tq_gemv_grouped(ms, x, ys=ys, stream=stream)
+                b.record(stream)
+        torch.cuda.synchronize()
+        if rep == 1:
+            durations = [a.elapsed_time(b) for a, b in ev]
+    avg_ms = sum(durations) / len(durations)
+    bytes_per_launch = step_bytes / len(launches)
+    achieved = bytes_per_launch / (avg_ms * 1e-3) / 1e9
+
+    result = {
+        "metric": "packed ternary GEMV HBM GB/s (% of peak) + us per Qwen3-8B decode-step linears",
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "us_per_step": round(ms_per_step * 1e3, 2),
+        "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp16 activations x base-3 packed ternary weights, fp32 accumulation",
+        "data": "synthetic (seeded; Qwen3-8B projection shapes, 10% two-plane groups)",
+        "config": {
+            "workload": f"Qwen3-8B decode-step linear stack, batch 1: {args.layers} layers x "
+                        "{q,k,v,o,gate,up,down}, 144 launches per step (q+k+v and gate+up grouped), HIP graph",
+            "layers": args.layers,
+            "launches_per_step": len(launches),
+            "weights_per_step": n_weights,
+            "packed_weight_bytes": weight_bytes,
+            "algorithmic_bytes_per_step": step_bytes,
+            "stored_bits_per_weight": round(8 * weight_bytes / n_weights, 4),
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "gemv_kernel",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "avg_launch_us": round(avg_ms * 1e3, 3),
+            "bytes_per_launch": round(bytes_per_launch, 1),
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample ...")
+        result["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,174 @@
+/*
+ * tq.h — packed ternary GEMV for AMD Instinct MI355X (gfx950): C ABI.
+ *
+ * The operation (paper arXiv 2609.09240, section 3, eq. 3, and the footnote
+ * to section 3): a linear projection is stored as
+ *     W^ = (mu + a0*T0 + a1*T1) (.) M,   T_i in {-1, 0, +1},
+ * where every 128-wide group of a row carries plane T0 with an fp16 scale
+ * s0, and a selected subset of groups also carries plane T1 with an fp16
+ * offset mu and an fp16 scale s1.  On such a two-plane group every weight is
+ * mu + s0*t0 + s1*t1; elsewhere it is s0*t0.  Activations stay fp16 (A16,
+ * section 3).  The packed format persists the discrete supports losslessly
+ * (section 12): five trits per byte as a base-3 code.
+ *
+ * ------------------------------------------------------------------------
+ * Packed format (the paper fixes no byte layout; this is the library's).
+ *
+ *   Group: 128 trits t[0..127] of one row, input indices 128g .. 128g+127.
+ *   Code byte j (j = 0..25) holds trits 5j .. 5j+4:
+ *       code = sum_{i=0..4} (t[5j+i] + 1) * 3^i          (0 .. 242)
+ *   Byte 25 holds t[125..127] in digits 0..2; its digits 3 and 4 are 1
+ *   (trit 0), so a valid last byte lies in 108..134.  Codes 243..255 are
+ *   invalid.
+ *   A code buffer of n groups is 26*n bytes in the "split" layout: bytes
+ *   0..23 of group f at offset 24*f, bytes 24 and 25 of group f at offset
+ *   24*n + 2*f.  (Every group body is 8-byte aligned for vector loads.)
+ *
+ *   A packed linear of N outputs and K inputs (K % 128 == 0, G = K/128):
+ *     codes0   uint8  [26*N*G]   plane 0, groups in row-major (r, g) order
+ *     scale0   fp16   [N][G]     s0
+ *     rowptr1  int32  [N+1]      CSR over rows of the two-plane groups
+ *     gidx1    uint16 [nnz1]     group index of each record; strictly
+ *                                increasing within a row
+ *     codes1   uint8  [26*nnz1]  plane 1 of each record (split layout)
+ *     offset1  fp16   [nnz1]     mu
+ *     scale1   fp16   [nnz1]     s1
+ *
+ * ------------------------------------------------------------------------
+ * Conventions for every entry point.
+ *
+ *   - Pointers to data are DEVICE pointers (hipMalloc / torch tensors on
+ *     the GPU) unless stated otherwise; tq_matrix itself lives in host
+ *     memory and is read only during the call.  The caller owns every
+ *     buffer; the library keeps no state and allocates no memory.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Every call is
+ *     asynchronous on that stream; nothing synchronises.
+ *   - Argument errors (NULL pointers, bad sizes or alignment, group != 128)
+ *     are detected on the host before anything is launched and returned
+ *     synchronously.  A failed launch returns TQ_ERR_HIP.
+ *   - Data errors (invalid trits or codes) are reported asynchronously
+ *     through an optional device counter `d_err` (int32, may be NULL),
+ *     which is incremented, never reset, by the number of bad bytes.
+ *   - tq_gemv, tq_gemv_grouped and tq_gemm_smallbatch do not validate codes:
+ *     invalid codes give unspecified (but finite-time, in-bounds) results.
+ *     Validate a matrix once with tq_validate when it is loaded.
+ *   - Results are deterministic: the same inputs give bit-identical outputs
+ *     on every run.
+ *   - Fp16 values are passed as their uint16 bit patterns.
+ */
+#ifndef TQ_H
+#define TQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TQ_ABI_VERSION 1
+#define TQ_GROUP 128
+#define TQ_GROUP_BYTES 26
+#define TQ_MAX_GROUPS_PER_ROW 256    /* K <= 32768 */
+#define TQ_MAX_GROUPED 8             /* matrices per tq_gemv_grouped call */
+#define TQ_MAX_BATCH 64              /* rows of X in tq_gemm_smallbatch */
+
+/* Output element type for tq_gemv / tq_gemm_smallbatch (the `flags` word). */
+#define TQ_OUT_FP16 0   /* fp16, rounded to nearest even from fp32 */
+#define TQ_OUT_FP32 1   /* the fp32 accumulator, unrounded */
+
+typedef enum {
+  TQ_OK = 0,
+  TQ_ERR_NULL = 1,        /* a required pointer is NULL */
+  TQ_ERR_SHAPE = 2,       /* a size is out of range or inconsistent */
+  TQ_ERR_ALIGN = 3,       /* a pointer is not aligned as required */
+  TQ_ERR_UNSUPPORTED = 4, /* a valid request this build does not support */
+  TQ_ERR_HIP = 5          /* the HIP runtime reported an error */
+} tq_status;
+
+/* Non-owning view of one packed linear (layout above).  When nnz1 == 0 the
+ * plane-1 pointers are ignored and may be NULL. */
+typedef struct tq_matrix {
+  int64_t n_out;            /* N >= 1 */
+  int64_t n_in;             /* K >= 128, K % 128 == 0, K/128 <= TQ_MAX_GROUPS_PER_ROW */
+  int32_t group;            /* must be 128 */
+  int32_t reserved;         /* must be 0 */
+  const uint8_t* codes0;    /* 8-byte aligned */
+  const uint16_t* scale0;   /* 2-byte aligned */
+  int64_t nnz1;             /* 0 <= nnz1 <= N*G */
+  const int32_t* rowptr1;   /* 4-byte aligned; rowptr1[0] == 0, rowptr1[N] == nnz1 */
+  const uint16_t* gidx1;
+  const uint8_t* codes1;    /* 8-byte aligned */
+  const uint16_t* offset1;
+  const uint16_t* scale1;
+} tq_matrix;
+
+/* Version of this ABI (TQ_ABI_VERSION). */
+int tq_abi_version(void);
+
+/* Static, human-readable name of a status code. */
+const char* tq_status_string(tq_status status);
+
+/* Encode trits to lattice codes (section 12: lossless encoding of the
+ * discrete supports).
+ *   trits   int8 [n_groups][128], values in {-1, 0, +1}
+ *   codes   uint8 [26*n_groups], split layout; 8-byte aligned
+ *   n_groups >= 0 (0 is a no-op); group must be 128.
+ * A code byte whose five trits include a value outside {-1, 0, +1} is
+ * written as 0xFF and counted in *d_err. */
+tq_status tq_pack(const int8_t* trits, int64_t n_groups, int32_t group,
+                  uint8_t* codes, int32_t* d_err, void* stream);
+
+/* Decode lattice codes to trits (inverse of tq_pack; bit-exact).
+ *   codes   uint8 [26*n_groups], split layout; 8-byte aligned
+ *   trits   int8 [n_groups][128]
+ * A code above 242 decodes to five zero trits and is counted in *d_err.
+ * The pad digits of byte 25 are not inspected (see tq_validate). */
+tq_status tq_unpack(const uint8_t* codes, int64_t n_groups, int32_t group,
+                    int8_t* trits, int32_t* d_err, void* stream);
+
+/* Count invalid bytes of a code buffer into *d_err (required here): codes
+ * above 242, and last bytes (byte 25) whose pad digits are not both 1. */
+tq_status tq_validate(const uint8_t* codes, int64_t n_groups, int32_t group,
+                      int32_t* d_err, void* stream);
+
+/* Dense fp16 dequantisation of a packed linear (eq. 3).
+ *   w  fp16 [N][K] row-major; 16-byte aligned
+ * Each weight is evaluated in fp32 in the fixed order
+ *     a = +0;  a += mu;  a += s0*t0;  a += s1*t1
+ * (mu and s1 only on two-plane groups; s*t is exact) and rounded once to
+ * fp16, nearest-even, so the result is bit-exact and unique. */
+tq_status tq_unpack_fp16(const tq_matrix* m, uint16_t* w, void* stream);
+
+/* y = W^ x for one fp16 activation vector (the decode-time GEMV).
+ *   x  fp16 [K]; 16-byte aligned
+ *   y  [N], fp16 (flags = TQ_OUT_FP16) or fp32 (TQ_OUT_FP32); 4-byte aligned
+ * Accumulates sign-selected fp16 activations in fp32, applies s0 per group
+ * and mu*sum(x_g) + s1*sum(t1*x_g) per two-plane group.  Accuracy:
+ * |y - exact| <= 2e-3 * sum_g (|s0| + [two-plane](|mu| + |s1|)) * ||x_g||_1
+ * per output.  x and y must not overlap the matrix buffers. */
+tq_status tq_gemv(const tq_matrix* m, const uint16_t* x, void* y,
+                  int32_t flags, void* stream);
+
+/* Several GEMVs that read the same x in one launch (e.g. q, k and v, or
+ * gate and up of one decoder layer).
+ *   ms  host array of n matrices (1 <= n <= TQ_MAX_GROUPED), all with the
+ *       same K
+ *   ys  host array of n device output pointers, ys[i] of N_i elements
+ * Each ys[i] equals what tq_gemv(&ms[i], x, ys[i], flags) produces,
+ * bit for bit. */
+tq_status tq_gemv_grouped(const tq_matrix* ms, int32_t n, const uint16_t* x,
+                          void* const* ys, int32_t flags, void* stream);
+
+/* Y = X W^T for a small batch of activations (paper section 18 lists kernel
+ * work across batch sizes as the next step).
+ *   X  fp16 [B][K] row-major; 16-byte aligned; 1 <= B <= TQ_MAX_BATCH
+ *   Y  [B][N] row-major, fp16 or fp32 per flags; 4-byte aligned
+ * Same accuracy bound as tq_gemv for every (b, r). */
+tq_status tq_gemm_smallbatch(const tq_matrix* m, const uint16_t* X, int32_t B,
+                             void* Y, int32_t flags, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TQ_H */

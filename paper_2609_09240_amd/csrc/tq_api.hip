@@ -1,0 +1,161 @@
+// Host entry points of libtq.so (declared in include/tq.h): argument checks
+// on the host, then one asynchronous launch on the caller's stream.
+//
+// Every check runs before the first HIP call, so an argument error is
+// returned synchronously and touches neither the device nor the stream.
+
+#include <stdint.h>
+
+#include "tq_internal.h"
+
+namespace {
+
+using tq::MatDev;
+
+inline bool misaligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; }
+
+inline tq_status from_hip(hipError_t e) { return e == hipSuccess ? TQ_OK : TQ_ERR_HIP; }
+
+tq_status check_codes_call(const void* codes, const void* other, int64_t n_groups, int32_t group) {
+  if (group != TQ_GROUP) return TQ_ERR_UNSUPPORTED;
+  if (n_groups < 0) return TQ_ERR_SHAPE;
+  if (n_groups > (INT64_MAX / 256)) return TQ_ERR_SHAPE;
+  if (n_groups == 0) return TQ_OK;
+  if (codes == nullptr || other == nullptr) return TQ_ERR_NULL;
+  if (misaligned(codes, 8)) return TQ_ERR_ALIGN;
+  return TQ_OK;
+}
+
+// Checks one matrix view and fills its device-side form.
+tq_status check_matrix(const tq_matrix* m, MatDev* d) {
+  if (m == nullptr) return TQ_ERR_NULL;
+  if (m->group != TQ_GROUP) return TQ_ERR_UNSUPPORTED;
+  if (m->reserved != 0) return TQ_ERR_SHAPE;
+  if (m->n_out < 1 || m->n_out > INT32_MAX) return TQ_ERR_SHAPE;
+  if (m->n_in < TQ_GROUP || m->n_in % TQ_GROUP != 0) return TQ_ERR_SHAPE;
+  const int64_t G = m->n_in / TQ_GROUP;
+  if (G > TQ_MAX_GROUPS_PER_ROW) return TQ_ERR_UNSUPPORTED;
+  if (m->codes0 == nullptr || m->scale0 == nullptr) return TQ_ERR_NULL;
+  if (misaligned(m->codes0, 8) || misaligned(m->scale0, 2)) return TQ_ERR_ALIGN;
+  if (m->nnz1 < 0 || m->nnz1 > m->n_out * G) return TQ_ERR_SHAPE;
+  if (m->nnz1 > 0) {
+    if (m->rowptr1 == nullptr || m->gidx1 == nullptr || m->codes1 == nullptr || m->offset1 == nullptr ||
+        m->scale1 == nullptr)
+      return TQ_ERR_NULL;
+    if (misaligned(m->rowptr1, 4) || misaligned(m->gidx1, 2) || misaligned(m->codes1, 8) ||
+        misaligned(m->offset1, 2) || misaligned(m->scale1, 2))
+      return TQ_ERR_ALIGN;
+  }
+  d->codes0 = m->codes0;
+  d->scale0 = m->scale0;
+  d->nnz1 = m->nnz1;
+  d->rowptr1 = m->nnz1 > 0 ? m->rowptr1 : nullptr;
+  d->gidx1 = m->nnz1 > 0 ? m->gidx1 : nullptr;
+  d->codes1 = m->nnz1 > 0 ? m->codes1 : nullptr;
+  d->offset1 = m->nnz1 > 0 ? m->offset1 : nullptr;
+  d->scale1 = m->nnz1 > 0 ? m->scale1 : nullptr;
+  d->n_out = (int32_t)m->n_out;
+  d->n_groups = (int32_t)G;
+  return TQ_OK;
+}
+
+tq_status check_flags(int32_t flags) {
+  return (flags == TQ_OUT_FP16 || flags == TQ_OUT_FP32) ? TQ_OK : TQ_ERR_UNSUPPORTED;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tq_abi_version(void) { return TQ_ABI_VERSION; }
+
+const char* tq_status_string(tq_status s) {
+  switch (s) {
+    case TQ_OK: return "TQ_OK";
+    case TQ_ERR_NULL: return "TQ_ERR_NULL: a required pointer is NULL";
+    case TQ_ERR_SHAPE: return "TQ_ERR_SHAPE: a size is out of range or inconsistent";
+    case TQ_ERR_ALIGN: return "TQ_ERR_ALIGN: a pointer is not aligned as required";
+    case TQ_ERR_UNSUPPORTED: return "TQ_ERR_UNSUPPORTED: request not supported by this build";
+    case TQ_ERR_HIP: return "TQ_ERR_HIP: the HIP runtime reported an error";
+  }
+  return "unknown tq_status";
+}
+
+tq_status tq_pack(const int8_t* trits, int64_t n_groups, int32_t group, uint8_t* codes, int32_t* d_err,
+                  void* stream) {
+  tq_status st = check_codes_call(codes, trits, n_groups, group);
+  if (st != TQ_OK || n_groups == 0) return st;
+  return from_hip(tq::launch_pack(trits, n_groups, codes, d_err, (hipStream_t)stream));
+}
+
+tq_status tq_unpack(const uint8_t* codes, int64_t n_groups, int32_t group, int8_t* trits, int32_t* d_err,
+                    void* stream) {
+  tq_status st = check_codes_call(codes, trits, n_groups, group);
+  if (st != TQ_OK || n_groups == 0) return st;
+  return from_hip(tq::launch_unpack(codes, n_groups, trits, d_err, (hipStream_t)stream));
+}
+
+tq_status tq_validate(const uint8_t* codes, int64_t n_groups, int32_t group, int32_t* d_err, void* stream) {
+  tq_status st = check_codes_call(codes, d_err, n_groups, group);
+  if (st != TQ_OK || n_groups == 0) return st;
+  if (misaligned(d_err, 4)) return TQ_ERR_ALIGN;
+  return from_hip(tq::launch_validate(codes, n_groups, d_err, (hipStream_t)stream));
+}
+
+tq_status tq_unpack_fp16(const tq_matrix* m, uint16_t* w, void* stream) {
+  MatDev d;
+  tq_status st = check_matrix(m, &d);
+  if (st != TQ_OK) return st;
+  if (w == nullptr) return TQ_ERR_NULL;
+  if (misaligned(w, 16)) return TQ_ERR_ALIGN;
+  return from_hip(tq::launch_unpack_fp16(d, w, (hipStream_t)stream));
+}
+
+tq_status tq_gemv(const tq_matrix* m, const uint16_t* x, void* y, int32_t flags, void* stream) {
+  MatDev d;
+  tq_status st = check_matrix(m, &d);
+  if (st != TQ_OK) return st;
+  if ((st = check_flags(flags)) != TQ_OK) return st;
+  if (x == nullptr || y == nullptr) return TQ_ERR_NULL;
+  if (misaligned(x, 16) || misaligned(y, 4)) return TQ_ERR_ALIGN;
+  void* ys[1] = {y};
+  return from_hip(tq::launch_gemv(&d, ys, 1, x, flags == TQ_OUT_FP32, (hipStream_t)stream));
+}
+
+tq_status tq_gemv_grouped(const tq_matrix* ms, int32_t n, const uint16_t* x, void* const* ys, int32_t flags,
+                          void* stream) {
+  if (ms == nullptr || ys == nullptr || x == nullptr) return TQ_ERR_NULL;
+  if (n < 1 || n > TQ_MAX_GROUPED) return TQ_ERR_SHAPE;
+  tq_status st = check_flags(flags);
+  if (st != TQ_OK) return st;
+  MatDev d[TQ_MAX_GROUPED];
+  int64_t total_rows = 0;
+  for (int i = 0; i < n; ++i) {
+    if ((st = check_matrix(&ms[i], &d[i])) != TQ_OK) return st;
+    if (ms[i].n_in != ms[0].n_in) return TQ_ERR_SHAPE;
+    if (ys[i] == nullptr) return TQ_ERR_NULL;
+    if (misaligned(ys[i], 4)) return TQ_ERR_ALIGN;
+    total_rows += ms[i].n_out;
+  }
+  if (total_rows > INT32_MAX) return TQ_ERR_SHAPE;
+  if (misaligned(x, 16)) return TQ_ERR_ALIGN;
+  return from_hip(tq::launch_gemv(d, ys, n, x, flags == TQ_OUT_FP32, (hipStream_t)stream));
+}
+
+tq_status tq_gemm_smallbatch(const tq_matrix* m, const uint16_t* X, int32_t B, void* Y, int32_t flags,
+                             void* stream) {
+  MatDev d;
+  tq_status st = check_matrix(m, &d);
+  if (st != TQ_OK) return st;
+  if ((st = check_flags(flags)) != TQ_OK) return st;
+  if (X == nullptr || Y == nullptr) return TQ_ERR_NULL;
+  if (B < 1 || B > TQ_MAX_BATCH) return TQ_ERR_SHAPE;
+  if (misaligned(X, 16) || misaligned(Y, 4)) return TQ_ERR_ALIGN;
+  if (B == 1) {
+    void* ys[1] = {Y};
+    return from_hip(tq::launch_gemv(&d, ys, 1, X, flags == TQ_OUT_FP32, (hipStream_t)stream));
+  }
+  return from_hip(tq::launch_gemm_smallbatch(d, X, B, Y, flags == TQ_OUT_FP32, (hipStream_t)stream));
+}
+
+}  // extern "C"

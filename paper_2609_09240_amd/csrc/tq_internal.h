@@ -1,0 +1,48 @@
+// Internal interface between the host entry points (tq_api.cpp) and the
+// kernel launchers (codec.hip, gemv.hip, gemm.hip).  Every launcher assumes
+// its arguments were already checked on the host and returns the status of
+// the launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/tq.h"
+
+namespace tq {
+
+constexpr int kGroup = TQ_GROUP;            // trits per group
+constexpr int kGroupBytes = TQ_GROUP_BYTES; // code bytes per group
+constexpr int kMainBytes = 24;              // bytes 0..23 (main region)
+
+// Device-side view of one packed linear (row counts fit in int32 here; the
+// host rejects larger matrices).
+struct MatDev {
+  const uint8_t* codes0;
+  const uint16_t* scale0;
+  const int32_t* rowptr1;
+  const uint16_t* gidx1;
+  const uint8_t* codes1;
+  const uint16_t* offset1;
+  const uint16_t* scale1;
+  int64_t nnz1;
+  int32_t n_out;
+  int32_t n_groups;   // groups per row, K / 128
+};
+
+hipError_t launch_pack(const int8_t* trits, int64_t n_groups, uint8_t* codes,
+                       int32_t* d_err, hipStream_t s);
+hipError_t launch_unpack(const uint8_t* codes, int64_t n_groups, int8_t* trits,
+                         int32_t* d_err, hipStream_t s);
+hipError_t launch_validate(const uint8_t* codes, int64_t n_groups,
+                           int32_t* d_err, hipStream_t s);
+hipError_t launch_unpack_fp16(const MatDev& m, uint16_t* w, hipStream_t s);
+
+// n matrices sharing x (all with the same n_groups).
+hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n,
+                       const uint16_t* x, bool out_f32, hipStream_t s);
+
+hipError_t launch_gemm_smallbatch(const MatDev& m, const uint16_t* X, int B,
+                                  void* Y, bool out_f32, hipStream_t s);
+
+}  // namespace tq

@@ -1,0 +1,257 @@
+"""ctypes binding of libtq.so — argument marshalling only.
+
+Each function has the name of the C entry point it calls (include/tq.h) and
+takes torch tensors that already live on the GPU; torch provides device
+memory and the current HIP stream, every step of the computation runs in the
+library's kernels.  There is no fallback: if libtq.so is missing, every call
+raises.
+"""
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtq.so")
+
+GROUP = 128
+GROUP_BYTES = 26
+OUT_FP16 = 0
+OUT_FP32 = 1
+MAX_GROUPED = 8
+MAX_BATCH = 64
+
+STATUS = {0: "TQ_OK", 1: "TQ_ERR_NULL", 2: "TQ_ERR_SHAPE", 3: "TQ_ERR_ALIGN",
+          4: "TQ_ERR_UNSUPPORTED", 5: "TQ_ERR_HIP"}
+
+
+class TqError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)}")
+
+
+class TqMatrix(ctypes.Structure):
+    _fields_ = [
+        ("n_out", ctypes.c_int64),
+        ("n_in", ctypes.c_int64),
+        ("group", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+        ("codes0", ctypes.c_void_p),
+        ("scale0", ctypes.c_void_p),
+        ("nnz1", ctypes.c_int64),
+        ("rowptr1", ctypes.c_void_p),
+        ("gidx1", ctypes.c_void_p),
+        ("codes1", ctypes.c_void_p),
+        ("offset1", ctypes.c_void_p),
+        ("scale1", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        mp = ctypes.POINTER(TqMatrix)
+        sigs = {
+            "tq_abi_version": ([], ctypes.c_int),
+            "tq_status_string": ([ctypes.c_int], ctypes.c_char_p),
+            "tq_pack": ([vp, i64, i32, vp, vp, vp], ctypes.c_int),
+            "tq_unpack": ([vp, i64, i32, vp, vp, vp], ctypes.c_int),
+            "tq_validate": ([vp, i64, i32, vp, vp], ctypes.c_int),
+            "tq_unpack_fp16": ([mp, vp, vp], ctypes.c_int),
+            "tq_gemv": ([mp, vp, vp, i32, vp], ctypes.c_int),
+            "tq_gemv_grouped": ([mp, i32, vp, ctypes.POINTER(ctypes.c_void_p), i32, vp], ctypes.c_int),
+            "tq_gemm_smallbatch": ([mp, vp, i32, vp, i32, vp], ctypes.c_int),
+        }
+        for name, (args, res) in sigs.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(status, where):
+    if status != 0:
+        raise TqError(status, where)
+
+
+def _cuda(t, dtype, name):
+    if not (t.is_cuda and t.dtype == dtype and t.is_contiguous()):
+        raise ValueError(f"{name} must be a contiguous {dtype} tensor on the GPU")
+
+
+# --------------------------------------------------------------------------
+# Device-resident packed linear.
+# --------------------------------------------------------------------------
+
+@dataclass
+class PackedLinear:
+    """A packed linear in device memory (the buffers tq_matrix points at)."""
+    n_out: int
+    n_in: int
+    codes0: torch.Tensor          # uint8 [26 * N * G]
+    scale0: torch.Tensor          # float16 [N, G]
+    rowptr1: torch.Tensor = None  # int32 [N + 1]
+    gidx1: torch.Tensor = None    # int16 [nnz1] (uint16 values)
+    codes1: torch.Tensor = None   # uint8 [26 * nnz1]
+    offset1: torch.Tensor = None  # float16 [nnz1]
+    scale1: torch.Tensor = None   # float16 [nnz1]
+
+    @property
+    def nnz1(self):
+        return 0 if self.gidx1 is None else int(self.gidx1.numel())
+
+    @property
+    def n_groups(self):
+        return self.n_out * (self.n_in // GROUP)
+
+    def struct(self):
+        m = TqMatrix()
+        m.n_out, m.n_in, m.group, m.reserved = self.n_out, self.n_in, GROUP, 0
+        m.codes0 = self.codes0.data_ptr()
+        m.scale0 = self.scale0.data_ptr()
+        m.nnz1 = self.nnz1
+        if self.nnz1:
+            m.rowptr1 = self.rowptr1.data_ptr()
+            m.gidx1 = self.gidx1.data_ptr()
+            m.codes1 = self.codes1.data_ptr()
+            m.offset1 = self.offset1.data_ptr()
+            m.scale1 = self.scale1.data_ptr()
+        return m
+
+    def nbytes(self):
+        """Bytes of the packed weights (codes, scales, plane-1 records, CSR)."""
+        ng = self.n_groups
+        b = GROUP_BYTES * ng + 2 * ng
+        if self.nnz1:
+            b += 4 * (self.n_out + 1) + 32 * self.nnz1
+        return b
+
+    @classmethod
+    def from_inputs(cls, inp, device="cuda", stream=None):
+        """Upload unpacked inputs (trits, scales, CSR) and pack them on the GPU."""
+        dev = torch.device(device)
+        t0 = torch.from_numpy(inp.t0.reshape(-1, GROUP)).to(dev)
+        codes0 = tq_pack(t0, stream=stream)
+        del t0
+        kw = {}
+        if inp.nnz1:
+            t1 = torch.from_numpy(inp.t1.reshape(-1, GROUP)).to(dev)
+            kw = dict(
+                rowptr1=torch.from_numpy(inp.rowptr1).to(dev),
+                gidx1=torch.from_numpy(inp.gidx1.view("int16")).to(dev),
+                codes1=tq_pack(t1, stream=stream),
+                offset1=torch.from_numpy(inp.mu1).to(dev),
+                scale1=torch.from_numpy(inp.s1).to(dev),
+            )
+        return cls(inp.n_out, inp.n_in, codes0, torch.from_numpy(inp.s0).to(dev), **kw)
+
+
+# --------------------------------------------------------------------------
+# Entry points (same names as the C ABI).
+# --------------------------------------------------------------------------
+
+def tq_abi_version():
+    return lib().tq_abi_version()
+
+
+def tq_status_string(status):
+    return lib().tq_status_string(status).decode()
+
+
+def tq_pack(trits, codes=None, d_err=None, stream=None):
+    """int8 trits [n, 128] -> uint8 codes [26 n] (split layout)."""
+    _cuda(trits, torch.int8, "trits")
+    n = trits.numel() // GROUP
+    if codes is None:
+        codes = torch.empty(GROUP_BYTES * n, dtype=torch.uint8, device=trits.device)
+    _check(lib().tq_pack(_ptr(trits), n, GROUP, _ptr(codes), _ptr(d_err), _stream(stream)), "tq_pack")
+    return codes
+
+
+def tq_unpack(codes, n_groups, trits=None, d_err=None, stream=None):
+    """uint8 codes [26 n] -> int8 trits [n, 128]."""
+    _cuda(codes, torch.uint8, "codes")
+    if trits is None:
+        trits = torch.empty((n_groups, GROUP), dtype=torch.int8, device=codes.device)
+    _check(lib().tq_unpack(_ptr(codes), n_groups, GROUP, _ptr(trits), _ptr(d_err), _stream(stream)),
+           "tq_unpack")
+    return trits
+
+
+def tq_validate(codes, n_groups, d_err=None, stream=None):
+    """Adds the number of invalid bytes to d_err (int32 [1]); returns d_err."""
+    _cuda(codes, torch.uint8, "codes")
+    if d_err is None:
+        d_err = torch.zeros(1, dtype=torch.int32, device=codes.device)
+    _check(lib().tq_validate(_ptr(codes), n_groups, GROUP, _ptr(d_err), _stream(stream)), "tq_validate")
+    return d_err
+
+
+def tq_unpack_fp16(mat, w=None, stream=None):
+    """Dense fp16 W^ [N, K] in the fixed fp32 evaluation order."""
+    if w is None:
+        w = torch.empty((mat.n_out, mat.n_in), dtype=torch.float16, device=mat.codes0.device)
+    m = mat.struct()
+    _check(lib().tq_unpack_fp16(ctypes.byref(m), _ptr(w), _stream(stream)), "tq_unpack_fp16")
+    return w
+
+
+def _out(n, shape, out_f32, device):
+    return torch.empty(shape, dtype=torch.float32 if out_f32 else torch.float16, device=device)
+
+
+def tq_gemv(mat, x, y=None, out_f32=False, stream=None):
+    """y = W^ x for fp16 x [K]; y fp16 [N] (or fp32)."""
+    _cuda(x, torch.float16, "x")
+    if y is None:
+        y = _out(mat.n_out, (mat.n_out,), out_f32, x.device)
+    m = mat.struct()
+    _check(lib().tq_gemv(ctypes.byref(m), _ptr(x), _ptr(y), OUT_FP32 if out_f32 else OUT_FP16,
+                         _stream(stream)), "tq_gemv")
+    return y
+
+
+def tq_gemv_grouped(mats, x, ys=None, out_f32=False, stream=None):
+    """[W_i^ x for each matrix] in one launch (all matrices share K)."""
+    _cuda(x, torch.float16, "x")
+    n = len(mats)
+    if ys is None:
+        ys = [_out(m.n_out, (m.n_out,), out_f32, x.device) for m in mats]
+    arr = (TqMatrix * n)(*[m.struct() for m in mats])
+    yp = (ctypes.c_void_p * n)(*[y.data_ptr() for y in ys])
+    _check(lib().tq_gemv_grouped(arr, n, _ptr(x), yp, OUT_FP32 if out_f32 else OUT_FP16,
+                                 _stream(stream)), "tq_gemv_grouped")
+    return ys
+
+
+def tq_gemm_smallbatch(mat, X, Y=None, out_f32=False, stream=None):
+    """Y = X W^T for fp16 X [B, K]; Y [B, N]."""
+    _cuda(X, torch.float16, "X")
+    B = X.shape[0]
+    if Y is None:
+        Y = _out(mat.n_out, (B, mat.n_out), out_f32, X.device)
+    m = mat.struct()
+    _check(lib().tq_gemm_smallbatch(ctypes.byref(m), _ptr(X), B, _ptr(Y), OUT_FP32 if out_f32 else OUT_FP16,
+                                    _stream(stream)), "tq_gemm_smallbatch")
+    return Y

@@ -1,0 +1,143 @@
+"""The C-ABI library loads and exports what include/tq.h declares (CPU only).
+
+Argument errors are detected on the host before any HIP call, so these
+tests exercise them without a GPU.  Calls use fake, well-aligned addresses
+that are never dereferenced; they only run where no GPU is visible, so a
+wrongly accepted call could never reach a device.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+from paper_2609_09240_amd import tq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tq.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(tq.LIB_PATH), reason="libtq.so not built")
+no_gpu = pytest.mark.skipif(torch.cuda.device_count() > 0, reason="fake-pointer calls run only without a GPU")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(tq_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for want in ["tq_pack", "tq_unpack", "tq_validate", "tq_unpack_fp16", "tq_gemv", "tq_gemv_grouped",
+                 "tq_gemm_smallbatch", "tq_status_string", "tq_abi_version"]:
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = ctypes.CDLL(tq.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_version_and_status_strings():
+    assert tq.tq_abi_version() == 1
+    for s in range(6):
+        assert tq.tq_status_string(s).startswith(tq.STATUS[s])
+    assert "unknown" in tq.tq_status_string(42)
+
+
+def test_matrix_struct_layout_matches_header():
+    # 2 x int64, 2 x int32, 2 pointers, int64, 5 pointers
+    assert ctypes.sizeof(tq.TqMatrix) == 8 * 2 + 4 * 2 + 8 * 2 + 8 + 8 * 5
+    assert tq.TqMatrix.nnz1.offset == 40
+
+
+FAKE = 0x7F0000000000   # 256-byte aligned, never dereferenced
+
+
+def _mat(**kw):
+    m = tq.TqMatrix()
+    m.n_out, m.n_in, m.group, m.reserved = 64, 256, 128, 0
+    m.codes0, m.scale0 = FAKE, FAKE + 0x100000
+    m.nnz1 = 0
+    for k, v in kw.items():
+        setattr(m, k, v)
+    return m
+
+
+def _gemv(m, x=FAKE + 0x200000, y=FAKE + 0x300000, flags=0):
+    return tq.lib().tq_gemv(ctypes.byref(m), ctypes.c_void_p(x), ctypes.c_void_p(y), flags, None)
+
+
+@no_gpu
+@pytest.mark.parametrize("kw,status", [
+    (dict(group=64), 4),
+    (dict(reserved=1), 2),
+    (dict(n_out=0), 2),
+    (dict(n_in=100), 2),
+    (dict(n_in=0), 2),
+    (dict(n_in=128 * 257), 4),
+    (dict(codes0=0), 1),
+    (dict(scale0=0), 1),
+    (dict(codes0=FAKE + 4), 3),
+    (dict(scale0=FAKE + 1), 3),
+    (dict(nnz1=-1), 2),
+    (dict(nnz1=64 * 2 + 1), 2),
+    (dict(nnz1=3), 1),                                    # plane-1 pointers missing
+    (dict(nnz1=3, rowptr1=FAKE + 2, gidx1=FAKE, codes1=FAKE, offset1=FAKE, scale1=FAKE), 3),
+    (dict(nnz1=3, rowptr1=FAKE, gidx1=FAKE, codes1=FAKE + 4, offset1=FAKE, scale1=FAKE), 3),
+])
+def test_gemv_rejects_bad_matrix(kw, status):
+    assert _gemv(_mat(**kw)) == status
+
+
+@no_gpu
+def test_gemv_rejects_bad_vectors_and_flags():
+    m = _mat()
+    assert _gemv(m, x=0) == 1
+    assert _gemv(m, y=0) == 1
+    assert _gemv(m, x=FAKE + 8) == 3
+    assert _gemv(m, y=FAKE + 2) == 3
+    assert _gemv(m, flags=7) == 4
+    assert tq.lib().tq_gemv(None, ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 0, None) == 1
+
+
+@no_gpu
+def test_codec_calls_reject_bad_arguments():
+    L = tq.lib()
+    v = ctypes.c_void_p
+    assert L.tq_pack(v(FAKE), 4, 64, v(FAKE), None, None) == 4
+    assert L.tq_pack(v(FAKE), -1, 128, v(FAKE), None, None) == 2
+    assert L.tq_pack(None, 4, 128, v(FAKE), None, None) == 1
+    assert L.tq_pack(v(FAKE), 4, 128, v(FAKE + 4), None, None) == 3
+    assert L.tq_pack(None, 0, 128, None, None, None) == 0          # empty input: no-op
+    assert L.tq_unpack(v(FAKE + 2), 4, 128, v(FAKE), None, None) == 3
+    assert L.tq_unpack(v(FAKE), 4, 128, None, None, None) == 1
+    assert L.tq_validate(v(FAKE), 4, 128, None, None) == 1          # counter required
+    assert L.tq_validate(v(FAKE), 4, 128, v(FAKE + 2), None) == 3
+
+
+@no_gpu
+def test_grouped_and_batch_reject_bad_arguments():
+    L = tq.lib()
+    v = ctypes.c_void_p
+    ms = (tq.TqMatrix * 3)(_mat(), _mat(n_in=512), _mat())
+    ys = (ctypes.c_void_p * 3)(FAKE, FAKE, FAKE)
+    assert L.tq_gemv_grouped(ms, 3, v(FAKE), ys, 0, None) == 2        # K differs
+    assert L.tq_gemv_grouped(ms, 0, v(FAKE), ys, 0, None) == 2
+    assert L.tq_gemv_grouped(ms, 9, v(FAKE), ys, 0, None) == 2
+    ys0 = (ctypes.c_void_p * 1)(0)
+    assert L.tq_gemv_grouped(ms, 1, v(FAKE), ys0, 0, None) == 1
+    m = _mat()
+    assert L.tq_gemm_smallbatch(ctypes.byref(m), v(FAKE), 0, v(FAKE), 0, None) == 2
+    assert L.tq_gemm_smallbatch(ctypes.byref(m), v(FAKE), 65, v(FAKE), 0, None) == 2
+    assert L.tq_gemm_smallbatch(ctypes.byref(m), v(FAKE + 2), 4, v(FAKE), 0, None) == 3
+    w = ctypes.c_void_p(FAKE + 8)
+    assert L.tq_unpack_fp16(ctypes.byref(m), w, None) == 3
+
+
+def test_binding_refuses_cpu_tensors():
+    with pytest.raises(ValueError):
+        tq.tq_pack(torch.zeros((2, 128), dtype=torch.int8))

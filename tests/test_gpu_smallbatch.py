@@ -1,0 +1,59 @@
+"""GPU parity of tq_gemm_smallbatch (LDS-decoded tiles + MFMA) against the
+fp64 oracle, per (batch row, output) within the same bound as the GEMV."""
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import Case, assert_within_bound, log
+from paper_2609_09240_amd import synth, tq
+
+pytestmark = pytest.mark.gpu
+
+
+def run(case, X, out_f32=False):
+    Y = tq.tq_gemm_smallbatch(case.gpu, torch.from_numpy(X).cuda(), out_f32=out_f32)
+    torch.cuda.synchronize()
+    return Y.cpu().numpy()
+
+
+@pytest.mark.parametrize("B", [1, 2, 4, 15, 16, 17, 33, 64])
+@pytest.mark.parametrize("n_out,n_in,f2", [(100, 512, 0.2), (64, 2560, 0.1), (1, 128, 1.0)])
+def test_small_shapes(B, n_out, n_in, f2):
+    case = Case(synth.linear(n_out, n_in, f2, (11, n_out, n_in, B)))
+    X = synth.activations(n_in, (11, n_out, n_in, 99), batch=B, outlier_frac=0.01)
+    got = run(case, X)
+    want = case.oracle_gemm(X)
+    r = assert_within_bound(got, want, case.bound(X), f"B={B} {n_out}x{n_in}")
+    log(f"smallbatch B={B} {n_out}x{n_in}: max err/bound {r:.3g}")
+
+
+@pytest.mark.parametrize("B", [1, 4, 16, 64])
+@pytest.mark.parametrize("name", ["gate", "down"])
+def test_mlp_shapes(B, name):
+    case = Case(synth.projection(name, layer=0, cfg=4))
+    X = synth.stage_activations(synth.STAGE_OF[name], layer=0, cfg=4, batch=B)
+    got = run(case, X, out_f32=True)
+    want = case.oracle_gemm(X)
+    r = assert_within_bound(got, want, case.bound(X), f"{name} B={B}")
+    log(f"smallbatch {name} B={B}: max err/bound {r:.3g}")
+
+
+def test_batch_rows_match_gemv():
+    case = Case(synth.projection("k", layer=2, cfg=4))
+    X = synth.stage_activations(0, layer=2, cfg=4, batch=8)
+    Y = run(case, X, out_f32=True)
+    for b in range(8):
+        y = tq.tq_gemv(case.gpu, torch.from_numpy(X[b].copy()).cuda(), out_f32=True)
+        torch.cuda.synchronize()
+        want = case.oracle_gemm(X[b:b + 1])[0]
+        bound = case.bound(X[b])
+        assert_within_bound(Y[b], want, bound, f"row {b}")
+        assert_within_bound(y.cpu().numpy(), want, bound, f"gemv row {b}")
+
+
+def test_deterministic():
+    case = Case(synth.linear(300, 1024, 0.1, (12, 0, 0, 0)))
+    X = synth.activations(1024, (12, 0, 0, 1), batch=24)
+    a, b = run(case, X, True), run(case, X, True)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
