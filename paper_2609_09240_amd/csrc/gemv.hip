@@ -6,38 +6,87 @@
 // kernel (section 13) is a prototype for another GPU and gives no design;
 // this one is built for CDNA4:
 //
-// * Lane ownership.  A workgroup of T threads covers RI = T / G rows per
-//   pass; thread t always owns group column g = t % G, so the 128
-//   activations of its group live in 78 VGPRs for the whole launch, laid out
-//   per code byte j as the fp16 pairs (x5j, x5j+1), (x5j+2, x5j+3),
-//   (x5j+4, 0).
-// * Decode.  A 256-entry table maps a code byte to the same three pairs of
-//   fp16 patterns (+1 = 0x3C00, -1 = 0xBC00, 0 = 0); three v_dot2_f32_f16
-//   then accumulate the sign-selected activations in fp32.  The table is
-//   replicated 16 times in LDS, copy q at byte offset 16 q of every 256-byte
-//   row, and lane t reads copy t % 16: the 16 lanes served together always
-//   hit 16 different bank quads, whatever codes they hold.
-// * Loads.  Group bodies (24 bytes, 8-aligned) arrive as three dwordx2
-//   loads, the two tail bytes as one ushort, the scale as one ushort; lanes
-//   of a row read consecutive groups, so every wave load is contiguous.
+// * Lane ownership.  A row of G groups is split into S = 2G half-groups: half
+//   h of group g holds code bytes 12h .. 12h+11 (inputs 60h .. 60h+59) plus
+//   tail byte 24+h (inputs 120+5h ..).  A workgroup of T threads covers
+//   RI = T / S rows per pass and thread t always owns half-group t % S, so its
+//   activations stay in 39 VGPRs for the whole launch, laid out per code byte
+//   j as the fp16 pairs (x5j, x5j+1), (x5j+2, x5j+3), (x5j+4, 0).
+// * Decode.  A 256-entry table maps a code to the same three pairs of fp16
+//   patterns (+1 = 0x3C00, -1 = 0xBC00, 0 = 0); three v_dot2_f32_f16 then
+//   accumulate the sign-selected activations in fp32.  The table is
+//   replicated kRep times in LDS (copy q of code c at byte 16 (kRep c + q)); a
+//   lane reads copy lane % kRep, so lanes served in the same LDS cycle hit
+//   different bank quads whatever codes they hold.  With kRep = 16 the table
+//   address (c << 8) | 16 q is one v_perm_b32 of the code dword.
+// * Loads.  Per pass a lane loads 12 body bytes (three dwords, 4-aligned in
+//   the split layout), its tail byte and its group's scale; lanes of a row
+//   read consecutive bytes, so every wave load is contiguous.  Loads run
+//   kDepth passes ahead of the decode (register ring), and each thread's
+//   first plane-1 record is loaded before the workgroup's set-up, so HBM
+//   latency overlaps the set-up and the plane-0 pass.
 // * Plane 1.  After the plane-0 pass over a block of rows has written
-//   s0 * p0 for every (row, group) into LDS, the block's two-plane records
-//   are processed densely (one record per thread) and each adds
-//   mu * sum(x_g) + s1 * sum(t1 * x_g) to its own (row, group) slot.
-// * Reduction.  Each row's G partials are summed by one wave: a fixed
+//   s0 * p0 for every (row, half-group) into LDS, the block's records are
+//   processed densely (one per thread) and each adds
+//   mu * sum(x_g) + s1 * sum(t1 * x_g) to its (row, group) slot.
+// * Reduction.  Each row's S partials are summed by one wave: a fixed
 //   strided sum per lane, then an xor butterfly of ds_swizzle steps and a
 //   cross-half readlane.  No atomics: results are bit-identical run to run.
 
 #include "tq_internal.h"
 
+#ifndef TQ_GEMV_REP
+#define TQ_GEMV_REP 4
+#endif
+#ifndef TQ_GEMV_DEPTH
+#define TQ_GEMV_DEPTH 2
+#endif
+
 namespace tq {
 namespace {
 
-constexpr int kRep = 16;                       // LUT copies (one per bank quad)
-constexpr int kLutEntries = 256 * kRep;        // 16-byte entries
-constexpr int kLutBytes = kLutEntries * 16;    // 64 KiB
-constexpr int kMaxThreads = 512;
+constexpr int kRep = TQ_GEMV_REP;              // LUT copies
+constexpr int kLutBytes = 256 * kRep * 16;
+constexpr int kDepth = TQ_GEMV_DEPTH;          // passes loaded ahead
+constexpr int kMaxThreads = 1024;
+constexpr int kHalfBytes = 12;                 // body bytes per half-group
+constexpr int kLaneBytes = kHalfBytes + 1;     // + one tail byte
+// x in LDS: group g at dword 65 g (130 halves).  The odd dword stride puts
+// the 64 lanes of a wave (32 groups x 2 halves) on different banks when they
+// read their activations.
+constexpr int kXStrideDw = 65;
 
+static_assert(kRep == 1 || kRep == 2 || kRep == 4 || kRep == 8 || kRep == 16, "kRep");
+
+// ---------------------------------------------------------------- table
+struct alignas(16) LutTable {
+  uint32_t v[256][4];
+};
+
+constexpr uint32_t pattern(int t) { return t > 0 ? 0x3C00u : (t < 0 ? 0xBC00u : 0u); }
+
+constexpr LutTable make_lut() {
+  LutTable L{};
+  for (int c = 0; c < 256; ++c) {
+    uint32_t t[5] = {0, 0, 0, 0, 0};
+    if (c < 243) {
+      int d = c;
+      for (int i = 0; i < 5; ++i) {
+        t[i] = pattern(d % 3 - 1);
+        d /= 3;
+      }
+    }
+    L.v[c][0] = t[0] | (t[1] << 16);
+    L.v[c][1] = t[2] | (t[3] << 16);
+    L.v[c][2] = t[4];
+    L.v[c][3] = 0;
+  }
+  return L;
+}
+
+__constant__ LutTable kLut = make_lut();
+
+// ---------------------------------------------------------------- params
 struct GemvParams {
   MatDev m[TQ_MAX_GROUPED];
   void* y[TQ_MAX_GROUPED];
@@ -45,7 +94,7 @@ struct GemvParams {
   int32_t rows_per_wg;
   int32_t n_mats;
   int32_t G;        // groups per row, shared by all matrices
-  int32_t ri;       // rows per pass = T / G
+  int32_t ri;       // rows per pass = T / (2G)
   int32_t rb_max;   // rows per LDS block
   int32_t out_f32;
 };
@@ -54,65 +103,58 @@ struct __attribute__((aligned(16))) U3 {
   uint32_t x, y, z;
 };
 
-__device__ inline uint32_t trit_pattern(int t) {
-  return t > 0 ? 0x3C00u : (t < 0 ? 0xBC00u : 0u);
-}
-
-// Entry e = code * kRep + copy, 16 bytes each: byte address code*256 + copy*16.
-__device__ inline void build_lut(uint4* lut, int tid, int nthreads) {
-  for (int e = tid; e < kLutEntries; e += nthreads) {
-    const int code = e / kRep;
-    uint4 v = {0u, 0u, 0u, 0u};
-    if (code < 243) {
-      int c = code, t[5];
-#pragma unroll
-      for (int i = 0; i < 5; ++i) {
-        t[i] = c % 3 - 1;
-        c /= 3;
-      }
-      v.x = trit_pattern(t[0]) | (trit_pattern(t[1]) << 16);
-      v.y = trit_pattern(t[2]) | (trit_pattern(t[3]) << 16);
-      v.z = trit_pattern(t[4]);
-    }
-    lut[e] = v;
-  }
-}
-
 __device__ inline float fdot2(uint32_t a, uint32_t b, float c) {
   typedef _Float16 h2 __attribute__((ext_vector_type(2)));
   return __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, a), __builtin_bit_cast(h2, b), c, false);
 }
 
-__device__ inline float h2f(uint16_t b) { return (float)__builtin_bit_cast(_Float16, b); }
+__device__ inline float h2f(uint32_t b) { return (float)__builtin_bit_cast(_Float16, (uint16_t)b); }
+
+template <int Pattern>
+__device__ inline float swz(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), Pattern));
+}
 
 // Sum over the 64 lanes of a wave; every lane returns the same value.
 __device__ inline float wave_sum(float v) {
-  v += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x041F));
-  v += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x081F));
-  v += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x101F));
-  v += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x201F));
-  v += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401F));
+  v += swz<0x041F>(v);   // xor 1
+  v += swz<0x081F>(v);   // xor 2
+  v += swz<0x101F>(v);   // xor 4
+  v += swz<0x201F>(v);   // xor 8
+  v += swz<0x401F>(v);   // xor 16
   const float lo = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
   const float hi = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
   return lo + hi;
 }
 
-// Code byte j (0..25) of a group whose body dwords are w[0..5] and whose two
-// tail bytes are the low half of w[6].
-__device__ inline uint32_t code_of(const uint32_t (&w)[7], int j) {
-  return (w[j >> 2] >> (8 * (j & 3))) & 0xFFu;
+// LDS byte address of this lane's table copy for byte B of dword w.
+template <int B>
+__device__ inline uint32_t lut_addr(uint32_t w, uint32_t slot) {
+  if constexpr (kRep == 16) {
+    // bytes [slot, code, 0, 0]: selector 4 picks byte 0 of `slot`, B byte B of w.
+    return __builtin_amdgcn_perm(slot, w, 0x0C0C0004u | (B << 8));
+  } else {
+    constexpr int sh = 4 + (kRep == 8 ? 3 : kRep == 4 ? 2 : kRep == 2 ? 1 : 0);
+    return (((w >> (8 * B)) & 0xFFu) << sh) | slot;
+  }
 }
 
-// Dot product of one group's trits (code dwords w) with activations laid
-// out as three fp16 pairs per code byte.
-template <typename XPairs>
-__device__ __attribute__((always_inline)) inline float group_dot(const unsigned char* lut_bytes, uint32_t slot16,
-                                  const uint32_t (&w)[7], XPairs xp) {
+// Dot product of NB code bytes (byte j in byte j % 4 of w[j / 4]) with the
+// activation pairs xp(j, q).
+template <int NB, typename W, typename XP>
+__device__ __attribute__((always_inline)) inline float code_dot(const unsigned char* lut, uint32_t slot,
+                                                                const W& w, XP xp) {
   float a0 = 0.f, a1 = 0.f, a2 = 0.f;
 #pragma unroll
-  for (int j = 0; j < kGroupBytes; ++j) {
-    const uint32_t addr = (code_of(w, j) << 8) | slot16;
-    const U3 p = *reinterpret_cast<const U3*>(lut_bytes + addr);
+  for (int j = 0; j < NB; ++j) {
+    uint32_t addr;
+    switch (j & 3) {
+      case 0: addr = lut_addr<0>(w[j >> 2], slot); break;
+      case 1: addr = lut_addr<1>(w[j >> 2], slot); break;
+      case 2: addr = lut_addr<2>(w[j >> 2], slot); break;
+      default: addr = lut_addr<3>(w[j >> 2], slot); break;
+    }
+    const U3 p = *reinterpret_cast<const U3*>(lut + addr);
     a0 = fdot2(p.x, xp(j, 0), a0);
     a1 = fdot2(p.y, xp(j, 1), a1);
     a2 = fdot2(p.z, xp(j, 2), a2);
@@ -120,25 +162,87 @@ __device__ __attribute__((always_inline)) inline float group_dot(const unsigned 
   return (a0 + a1) + a2;
 }
 
-__device__ inline void load_group(const uint8_t* body, const uint8_t* tail, uint32_t (&w)[7]) {
-  const uint2* b = reinterpret_cast<const uint2*>(body);
-  const uint2 w0 = b[0], w1 = b[1], w2 = b[2];
-  w[0] = w0.x; w[1] = w0.y; w[2] = w1.x; w[3] = w1.y; w[4] = w2.x; w[5] = w2.y;
-  w[6] = *reinterpret_cast<const uint16_t*>(tail);
+// One pass of plane 0 for one lane: 12 body bytes, 1 tail byte, 1 scale.
+struct Pass {
+  uint32_t w[4];   // w[0..2] body, w[3] tail byte
+  uint32_t sc;     // scale bits
+};
+
+__device__ inline void load_pass(Pass& p, const uint8_t* body, const uint8_t* tail, const uint16_t* scale) {
+  const uint32_t* b = reinterpret_cast<const uint32_t*>(body);
+  p.w[0] = __builtin_nontemporal_load(b);
+  p.w[1] = __builtin_nontemporal_load(b + 1);
+  p.w[2] = __builtin_nontemporal_load(b + 2);
+  p.w[3] = __builtin_nontemporal_load(tail);
+  p.sc = __builtin_nontemporal_load(scale);
 }
 
-__global__ void __launch_bounds__(kMaxThreads) gemv_kernel(const GemvParams P, const uint16_t* __restrict__ x) {
+// A plane-1 record: 24 body bytes, 2 tail bytes, group, offset, scale.
+struct Rec {
+  uint32_t w[7];
+  uint32_t g, mu, s1;
+};
+
+__device__ inline void load_rec(Rec& r, const MatDev& M, int64_t k) {
+  const uint2* b = reinterpret_cast<const uint2*>(M.codes1 + (int64_t)kMainBytes * k);
+  const uint2 b0 = b[0], b1 = b[1], b2 = b[2];
+  r.w[0] = b0.x; r.w[1] = b0.y; r.w[2] = b1.x; r.w[3] = b1.y; r.w[4] = b2.x; r.w[5] = b2.y;
+  r.w[6] = *reinterpret_cast<const uint16_t*>(M.codes1 + (int64_t)kMainBytes * M.nnz1 + 2 * k);
+  r.g = M.gidx1[k];
+  r.mu = M.offset1[k];
+  r.s1 = M.scale1[k];
+}
+
+// mu * sum(x_g) + s1 * sum(t1 x_g) of one record, activations from LDS.
+__device__ __attribute__((always_inline)) inline float record_value(const unsigned char* lut, uint32_t slot,
+                                                                    const uint16_t* xs, const float* gsum,
+                                                                    const Rec& rec, int G) {
+  const int gg = min((int)rec.g, G - 1);
+  float p1 = 0.f;
+#pragma unroll 1
+  for (int hh = 0; hh < 2; ++hh) {
+    const uint32_t hw[4] = {hh ? rec.w[3] : rec.w[0], hh ? rec.w[4] : rec.w[1], hh ? rec.w[5] : rec.w[2],
+                            (rec.w[6] >> (8 * hh)) & 0xFFu};
+    const uint32_t* xd = reinterpret_cast<const uint32_t*>(xs) + kXStrideDw * gg + 30 * hh;   // inputs 60 hh ..
+    const uint16_t* xt = xs + 2 * kXStrideDw * gg + 120 + 5 * hh;
+    p1 += code_dot<kLaneBytes>(lut, slot, hw, [&](int j, int q) -> uint32_t {
+      if (j < kHalfBytes) {
+        const int p = 5 * j + 2 * q;   // input offset within the half
+        if ((p & 1) == 0) return q < 2 ? xd[p / 2] : (xd[p / 2] & 0xFFFFu);
+        return q < 2 ? __builtin_amdgcn_alignbit(xd[(p + 1) / 2], xd[(p - 1) / 2], 16) : (xd[(p - 1) / 2] >> 16);
+      }
+      const int p = 2 * q;             // tail byte: inputs 120 + 5 hh + p
+      const uint32_t a = 120 + 5 * hh + p < kGroup ? (uint32_t)xt[p] : 0u;
+      const uint32_t b = (q < 2 && 121 + 5 * hh + p < kGroup) ? (uint32_t)xt[p + 1] : 0u;
+      return a | (b << 16);
+    });
+  }
+  return h2f(rec.mu) * gsum[gg] + h2f(rec.s1) * p1;
+}
+
+// kPasses: plane-0 passes per lane, all loaded up front.  kXLoads: 16-byte
+// loads of x per thread (ceil(K / 8 / T)).  Every global load of the
+// preamble is unconditional (out-of-range lanes load a valid address and
+// ignore it) and issued in the order the data is needed, so each wait is an
+// exact vmcnt and one memory round trip covers the set-up while the plane-0
+// bytes stream in behind it.
+template <int kPasses, int kXLoads>
+__global__ void __launch_bounds__(kMaxThreads) __attribute__((amdgpu_waves_per_eu(4)))
+gemv_kernel(const GemvParams P, const uint16_t* __restrict__ x) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int G = P.G;
+  const int S = 2 * G;
   const int K = G * kGroup;
-  unsigned char* lut_bytes = smem;
+  unsigned char* lut = smem;
   uint16_t* xs = reinterpret_cast<uint16_t*>(smem + kLutBytes);
-  float* gsum = reinterpret_cast<float*>(smem + kLutBytes + 2 * K);
+  uint32_t* xsw = reinterpret_cast<uint32_t*>(xs);
+  float* gsum = reinterpret_cast<float*>(smem + kLutBytes + 4 * kXStrideDw * G);
   int* rp = reinterpret_cast<int*>(gsum + G);
   float* part = reinterpret_cast<float*>(rp + P.rb_max + 1);
 
   const int tid = threadIdx.x;
   const int T = blockDim.x;
+  const int nw = T >> 6;
 
   // Which matrix this workgroup serves (constant indices only, so the
   // parameter block is never copied to scratch).
@@ -158,113 +262,197 @@ __global__ void __launch_bounds__(kMaxThreads) gemv_kernel(const GemvParams P, c
     }
   const int row_begin = ((int)blockIdx.x - wgb) * P.rows_per_wg;
   const int row_end = min(M.n_out, row_begin + P.rows_per_wg);
-
-  // Stage x and the decode table.
-  for (int i = tid; i < K / 8; i += T)
-    reinterpret_cast<uint4*>(xs)[i] = reinterpret_cast<const uint4*>(x)[i];
-  build_lut(reinterpret_cast<uint4*>(lut_bytes), tid, T);
-  __syncthreads();
-  for (int g = tid; g < G; g += T) {
-    float s = 0.f;
-    for (int i = 0; i < kGroup; ++i) s += h2f(xs[kGroup * g + i]);
-    gsum[g] = s;
-  }
+  const int nrb = row_end - row_begin;
 
   const int ri = P.ri;
-  const bool active = tid < ri * G;
-  const int g = active ? tid % G : 0;
-  const int rl = active ? tid / G : 0;
-  const uint32_t slot16 = (uint32_t)(tid & (kRep - 1)) << 4;
+  const bool active = tid < ri * S;
+  const int sl = active ? tid % S : 0;   // half-group slot within the row
+  const int g = sl >> 1;
+  const int h = sl & 1;
+  const int rl = active ? tid / S : 0;
+  const uint32_t slot = (uint32_t)(tid & (kRep - 1)) << 4;
+  const bool has_rec = M.nnz1 > 0;
 
-  // This thread's activations as three fp16 pairs per code byte.
-  uint32_t xr[kGroupBytes][3];
+  // 1. CSR slice and record range (loaded first: waiting for them waits for
+  //    nothing else).  Without records, x stands in as a readable address.
+  const int* rpp = has_rec ? M.rowptr1 + row_begin : reinterpret_cast<const int*>(x);
+  const int rp_mine = rpp[has_rec ? min(tid, nrb) : 0];
+  const int k0 = rpp[0];
+  const int k1 = rpp[has_rec ? nrb : 0];
+  // 2. x and the decode table.
+  uint4 xv[kXLoads];
+#pragma unroll
+  for (int q = 0; q < kXLoads; ++q) xv[q] = reinterpret_cast<const uint4*>(x)[min(tid + q * T, K / 8 - 1)];
+  const uint4 lutv = *reinterpret_cast<const uint4*>(kLut.v[min(tid, 255)]);
+  // 3. Every plane-0 pass of this lane.
+  const int64_t ngroups = (int64_t)M.n_out * G;
+  const uint8_t* body0 = M.codes0 + kHalfBytes * h;
+  const uint8_t* tail0 = M.codes0 + (int64_t)kMainBytes * ngroups + h;
+  Pass buf[kPasses];
+#pragma unroll
+  for (int d = 0; d < kPasses; ++d) {
+    const int r = min(row_begin + rl + d * ri, row_end - 1);
+    const int64_t f = (int64_t)r * G + g;
+    load_pass(buf[d], body0 + kMainBytes * f, tail0 + 2 * f, M.scale0 + f);
+  }
+  // 4. One record per thread, spread across the waves.
+  const int ri_rec = (tid & 63) * nw + (tid >> 6);
+  const int kr = k0 + ri_rec;
+  const bool rec_valid = has_rec && kr < k1 && kr >= 0 && (int64_t)kr < M.nnz1;
+  MatDev MR = M;
+  if (!has_rec) {   // readable stand-ins; the loaded values are ignored
+    MR.codes1 = M.codes0;
+    MR.gidx1 = MR.offset1 = MR.scale1 = M.scale0;
+  }
+  Rec rec;
+  load_rec(rec, MR, rec_valid ? kr : (has_rec ? (int)min((int64_t)max(k0, 0), M.nnz1 - 1) : 0));
+
+  // Set-up in LDS.
+#pragma unroll
+  for (int q = 0; q < kXLoads; ++q) {
+    const int i = tid + q * T;   // 8 halves: group i / 16, dwords 4 (i % 16) ..
+    if (i < K / 8) {
+      uint32_t* d = xsw + kXStrideDw * (i >> 4) + 4 * (i & 15);
+      d[0] = xv[q].x;
+      d[1] = xv[q].y;
+      d[2] = xv[q].z;
+      d[3] = xv[q].w;
+    }
+  }
+  if (tid < 256) {
+#pragma unroll
+    for (int q = 0; q < kRep; ++q) reinterpret_cast<uint4*>(lut)[tid * kRep + q] = lutv;
+  }
+  if (has_rec && tid <= nrb) rp[tid] = rp_mine;
+  __syncthreads();
+
+  // This lane's activations: 12 body bytes (inputs 60h + 5j ..) and the tail
+  // byte (inputs 120 + 5h ..), three fp16 pairs per byte.
+  uint32_t xr[kLaneBytes][3];
   {
-    const uint16_t* xg = xs + kGroup * g;
+    const uint32_t* xd = xsw + kXStrideDw * g + 30 * h;   // inputs 60 h ..
 #pragma unroll
-    for (int j = 0; j < kGroupBytes; ++j) {
+    for (int j = 0; j < kHalfBytes; j += 2) {   // bytes j, j+1: inputs 5j .. 5j+9 = dwords 5j/2 ..
+      const int q = 5 * j / 2;
+      const uint32_t d0 = xd[q], d1 = xd[q + 1], d2 = xd[q + 2], d3 = xd[q + 3], d4 = xd[q + 4];
+      xr[j][0] = d0;
+      xr[j][1] = d1;
+      xr[j][2] = d2 & 0xFFFFu;
+      xr[j + 1][0] = __builtin_amdgcn_alignbit(d3, d2, 16);
+      xr[j + 1][1] = __builtin_amdgcn_alignbit(d4, d3, 16);
+      xr[j + 1][2] = d4 >> 16;
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    const uint16_t* xt = xs + 2 * kXStrideDw * g + 120 + 5 * h;
+    uint32_t e[5];
 #pragma unroll
-      for (int q = 0; q < 3; ++q) {
-        const int p = 5 * j + 2 * q;
-        const uint32_t lo = p < kGroup ? xg[p] : 0u;
-        const uint32_t hi = (q < 2 && p + 1 < kGroup) ? xg[p + 1] : 0u;
-        xr[j][q] = lo | (hi << 16);
+    for (int i = 0; i < 5; ++i) e[i] = (120 + 5 * h + i < kGroup) ? (uint32_t)xt[i] : 0u;
+    xr[kHalfBytes][0] = e[0] | (e[1] << 16);
+    xr[kHalfBytes][1] = e[2] | (e[3] << 16);
+    xr[kHalfBytes][2] = e[4];
+  }
+  // Group sums for the offsets: each lane sums its half, the pair combines
+  // (half 0 first on both lanes, so both get the same bits).
+  {
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < kLaneBytes; ++j) {
+      s = fdot2(xr[j][0], 0x3C003C00u, s);
+      s = fdot2(xr[j][1], 0x3C003C00u, s);
+      s = fdot2(xr[j][2], 0x3C003C00u, s);
+    }
+    const float other = swz<0x041F>(s);
+    const float tot = h == 0 ? s + other : other + s;
+    if (active && rl == 0 && h == 0) gsum[g] = tot;
+  }
+
+  // Plane 0: part[row][slot] = s0 * sum_i t0 x over the half-group.
+#pragma unroll
+  for (int d = 0; d < kPasses; ++d) {
+    const float p = code_dot<kLaneBytes>(lut, slot, buf[d].w, [&](int j, int q) { return xr[j][q]; });
+    if (active && rl + d * ri < nrb) part[(rl + d * ri) * S + sl] = p * h2f(buf[d].sc);
+    __builtin_amdgcn_sched_barrier(0);   // keep passes apart: bounds the LUT reads in flight
+  }
+  // Plane-0 passes beyond kPasses (only when the host could not fit a
+  // matrix into one round of workgroups with kPasses passes).
+  for (int d = kPasses; active && rl + d * ri < nrb; ++d) {
+    const int64_t f = (int64_t)(row_begin + rl + d * ri) * G + g;
+    Pass q;
+    load_pass(q, body0 + kMainBytes * f, tail0 + 2 * f, M.scale0 + f);
+    const float p = code_dot<kLaneBytes>(lut, slot, q.w, [&](int j, int qq) { return xr[j][qq]; });
+    part[(rl + d * ri) * S + sl] = p * h2f(q.sc);
+  }
+
+  // Plane 1: each record adds to the (row, group) slot of half 0.
+  if (has_rec) {
+    __syncthreads();   // plane-0 partials and group sums are in LDS
+    for (int i = ri_rec, k = kr; k0 + i < k1; i += T, k += T) {
+      if (i != ri_rec) load_rec(rec, M, k);
+      if (k < 0 || (int64_t)k >= M.nnz1) break;
+      int lo = 0, hi = nrb - 1;   // last row whose first record is <= k
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (rp[mid] <= k) lo = mid; else hi = mid - 1;
       }
+      const float v = record_value(lut, slot, xs, gsum, rec, G);
+      float* dst = part + lo * S + 2 * min((int)rec.g, G - 1);
+      *dst = *dst + v;
     }
   }
   __syncthreads();
 
-  const int64_t ngroups = (int64_t)M.n_out * G;
-  const uint8_t* tails0 = M.codes0 + (int64_t)kMainBytes * ngroups;
-  const uint8_t* tails1 = M.codes1 + (int64_t)kMainBytes * M.nnz1;
-
-  for (int rb0 = row_begin; rb0 < row_end; rb0 += P.rb_max) {
-    const int rb1 = min(row_end, rb0 + P.rb_max);
-    const int nrb = rb1 - rb0;
-
-    // Plane 0: part[row][g] = s0 * sum_i t0 x.
-    if (active) {
-      for (int r = rb0 + rl; r < rb1; r += ri) {
-        const int64_t f = (int64_t)r * G + g;
-        uint32_t w[7];
-        load_group(M.codes0 + (int64_t)kMainBytes * f, tails0 + 2 * f, w);
-        const float s0 = h2f(M.scale0[f]);
-        const float p = group_dot(lut_bytes, slot16, w, [&](int j, int q) { return xr[j][q]; });
-        part[(r - rb0) * G + g] = p * s0;
-      }
+  // Row sums: each wave reduces rows wave, wave + nw, ... four at a time.
+  const int lane = tid & 63;
+  for (int r0 = tid >> 6; r0 < nrb; r0 += 4 * nw) {
+    float s[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int rr = r0 + u * nw;
+      s[u] = 0.f;
+      if (rr < nrb)
+        for (int q = lane; q < S; q += 64) s[u] += part[rr * S + q];
     }
-
-    // Plane 1: one record per thread, added to its own (row, group) slot.
-    if (M.nnz1 > 0) {
-      for (int i = tid; i <= nrb; i += T) rp[i] = M.rowptr1[rb0 + i];
-      __syncthreads();
-      // Clamped so that a malformed CSR cannot index outside the buffers.
-      const int k0 = max(rp[0], 0);
-      const int k1 = (int)min((int64_t)rp[nrb], M.nnz1);
-      for (int k = k0 + tid; k < k1; k += T) {
-        int lo = 0, hi = nrb - 1;   // last row whose first record is <= k
-        while (lo < hi) {
-          const int mid = (lo + hi + 1) >> 1;
-          if (rp[mid] <= k) lo = mid; else hi = mid - 1;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) s[u] = wave_sum(s[u]);
+    if (lane == 0) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int rr = r0 + u * nw;
+        if (rr < nrb) {
+          if (P.out_f32)
+            reinterpret_cast<float*>(yp)[row_begin + rr] = s[u];
+          else
+            reinterpret_cast<uint16_t*>(yp)[row_begin + rr] = __builtin_bit_cast(uint16_t, (_Float16)s[u]);
         }
-        const int gg = min((int)M.gidx1[k], G - 1);
-        uint32_t w[7];
-        load_group(M.codes1 + (int64_t)kMainBytes * k, tails1 + 2 * (int64_t)k, w);
-        const float mu = h2f(M.offset1[k]);
-        const float s1 = h2f(M.scale1[k]);
-        const uint16_t* xg = xs + kGroup * gg;
-        const float p1 = group_dot(lut_bytes, slot16, w, [&](int j, int q) {
-          const int p = 5 * j + 2 * q;
-          const uint32_t lo2 = p < kGroup ? xg[p] : 0u;
-          const uint32_t hi2 = (q < 2 && p + 1 < kGroup) ? xg[p + 1] : 0u;
-          return lo2 | (hi2 << 16);
-        });
-        float* slot = part + lo * G + gg;
-        *slot = *slot + (mu * gsum[gg] + s1 * p1);
       }
     }
-    __syncthreads();
-
-    // Row sums: one wave per row.
-    const int lane = tid & 63;
-    const int nw = T >> 6;
-    for (int rr = tid >> 6; rr < nrb; rr += nw) {
-      float s = 0.f;
-      for (int q = lane; q < G; q += 64) s += part[rr * G + q];
-      s = wave_sum(s);
-      if (lane == 0) {
-        if (P.out_f32)
-          reinterpret_cast<float*>(yp)[rb0 + rr] = s;
-        else
-          reinterpret_cast<uint16_t*>(yp)[rb0 + rr] = __builtin_bit_cast(uint16_t, (_Float16)s);
-      }
-    }
-    __syncthreads();
   }
+}
+
+typedef void (*GemvKernel)(const GemvParams, const uint16_t*);
+
+constexpr int kPassChoices[] = {1, 2, 3, 4};
+constexpr int kNumPass = 4;
+constexpr int kXChoices[] = {1, 2, 4};
+
+template <int PI, int XI>
+constexpr GemvKernel kernel_at() {
+  return gemv_kernel<kPassChoices[PI], kXChoices[XI]>;
+}
+
+GemvKernel select_kernel(int pi, int xi) {
+  static const GemvKernel table[kNumPass][3] = {
+      {kernel_at<0, 0>(), kernel_at<0, 1>(), kernel_at<0, 2>()},
+      {kernel_at<1, 0>(), kernel_at<1, 1>(), kernel_at<1, 2>()},
+      {kernel_at<2, 0>(), kernel_at<2, 1>(), kernel_at<2, 2>()},
+      {kernel_at<3, 0>(), kernel_at<3, 1>(), kernel_at<3, 2>()},
+  };
+  return table[pi][xi];
 }
 
 struct DeviceInfo {
   int cus = 0;
-  bool attr_set = false;
+  bool attr_set[kNumPass][3] = {};
 };
 
 DeviceInfo& device_info() {
@@ -275,9 +463,8 @@ DeviceInfo& device_info() {
 }
 
 size_t lds_bytes(int G, int rb_max) {
-  const int K = G * kGroup;
-  return (size_t)kLutBytes + 2 * (size_t)K + 4 * (size_t)G + 4 * (size_t)(rb_max + 1) +
-         4 * (size_t)rb_max * G;
+  return (size_t)kLutBytes + 4 * (size_t)kXStrideDw * G + 4 * (size_t)G + 4 * (size_t)(rb_max + 1) +
+         4 * (size_t)rb_max * 2 * G;
 }
 
 }  // namespace
@@ -292,43 +479,64 @@ hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n, const uint16_t*
     e = hipDeviceGetAttribute(&di.cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
   }
-  if (!di.attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemv_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (e != hipSuccess) return e;
-    di.attr_set = true;
-  }
 
   GemvParams P = {};
   const int G = ms[0].n_groups;
-  // Threads per workgroup: the multiple of 64 in [256, 512] that leaves the
-  // fewest lanes without a group column.
-  int T = 256, best_used = -1;
-  for (int t = 256; t <= kMaxThreads; t += 64) {
-    const int used = (t / G) * G;
-    if (used * (int64_t)T > (int64_t)best_used * t) {
-      best_used = used;
-      T = t;
-    }
-  }
-  const int ri = T / G;
+  const int S = 2 * G;
   int64_t total_rows = 0;
   for (int i = 0; i < n; ++i) total_rows += ms[i].n_out;
 
-  // LDS block: as many rows as fit beside the fixed arrays, preferring two
-  // workgroups per CU when they fit.
+  // LDS: table + x + group sums + CSR slice + partials.  Two workgroups per
+  // CU when they fit in half of the 160 KiB (then at most 512 threads each,
+  // 16 waves per CU in all); otherwise one of up to 1024 threads.
   const size_t fixed = lds_bytes(G, 0);
-  const size_t per_row = 4 * (size_t)G + 4;
-  const size_t two_per_cu = 80 * 1024, one_per_cu = 160 * 1024;
-  const int wgs_per_cu = fixed + per_row * ri <= two_per_cu ? 2 : 1;
-  const size_t budget = wgs_per_cu == 2 ? two_per_cu : one_per_cu;
-  const int target_wgs = di.cus * wgs_per_cu;
-  int rows_per_wg = (int)((total_rows + target_wgs - 1) / target_wgs);
-  rows_per_wg = ((rows_per_wg + ri - 1) / ri) * ri;
-  int rb_max = (int)((budget - fixed) / per_row);
-  rb_max = rb_max / ri * ri;
-  if (rb_max < ri) rb_max = ri;
-  if (rb_max > rows_per_wg) rb_max = rows_per_wg;
+  const size_t per_row = 8 * (size_t)G + 4;
+  const size_t half_lds = 80 * 1024, full_lds = 160 * 1024;
+  const int ri512 = 512 / S;
+  const int wgs_per_cu = (ri512 >= 1 && fixed + per_row * ri512 <= half_lds) ? 2 : 1;
+  const size_t budget = wgs_per_cu == 2 ? half_lds : full_lds;
+  const int t_max = wgs_per_cu == 2 ? 512 : kMaxThreads;
+
+  // Threads per workgroup: the multiple of 64 in [256, t_max] leaving the
+  // fewest lanes without a half-group; the larger wins ties.
+  int T = 0;
+  double best = -1.0;
+  for (int t = 256; t <= t_max; t += 64) {
+    const double used = (double)((t / S) * S) / t;
+    if (used >= best - 1e-9) {
+      best = used;
+      T = t;
+    }
+  }
+  const int ri = T / S;
+
+  // Passes per lane: enough for one round of workgroups, capped by the
+  // compiled choices, by LDS for the partials and by one CSR entry per thread.
+  int max_rows = (int)((budget - fixed) / per_row);
+  if (max_rows > T - 1) max_rows = T - 1;
+  const int max_pass = max_rows / ri < 1 ? 1 : max_rows / ri;
+  const int64_t target_wgs = (int64_t)di.cus * wgs_per_cu;
+  int want = (int)((total_rows + target_wgs * ri - 1) / (target_wgs * ri));
+  if (want > max_pass) want = max_pass;
+  int pi = 0;
+  while (pi < kNumPass - 1 && kPassChoices[pi] < want) ++pi;
+  int passes = kPassChoices[pi];
+  if (passes > max_pass) {   // largest compiled choice that fits
+    while (pi > 0 && kPassChoices[pi] > max_pass) --pi;
+    passes = kPassChoices[pi];
+  }
+  const int rows_per_wg = passes * ri;
+  const int xloads = (G * kGroup / 8 + T - 1) / T;
+  const int xi = xloads <= 1 ? 0 : (xloads <= 2 ? 1 : 2);
+  if (kXChoices[xi] < xloads) return hipErrorInvalidValue;
+
+  const GemvKernel kern = select_kernel(pi, xi);
+  if (!di.attr_set[pi][xi]) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    di.attr_set[pi][xi] = true;
+  }
 
   int wg = 0;
   for (int i = 0; i < n; ++i) {
@@ -342,9 +550,9 @@ hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n, const uint16_t*
   P.n_mats = n;
   P.G = G;
   P.ri = ri;
-  P.rb_max = rb_max;
+  P.rb_max = rows_per_wg;
   P.out_f32 = out_f32 ? 1 : 0;
-  hipLaunchKernelGGL(gemv_kernel, dim3(wg), dim3(T), lds_bytes(G, rb_max), s, P, x);
+  hipLaunchKernelGGL(kern, dim3(wg), dim3(T), lds_bytes(G, rows_per_wg), s, P, x);
   return hipGetLastError();
 }
 
