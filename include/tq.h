@@ -89,7 +89,9 @@ typedef enum {
  * plane-1 pointers are ignored and may be NULL. */
 typedef struct tq_matrix {
   int64_t n_out;            /* N >= 1 */
-  int64_t n_in;             /* K >= 128, K % 128 == 0, K/128 <= TQ_MAX_GROUPS_PER_ROW */
+  int64_t n_in;             /* K >= 128, K % 128 == 0, K/128 <= TQ_MAX_GROUPS_PER_ROW;
+                               26 * N * K/128 must be below 2^32 (codes of one
+                               matrix under 4 GiB) */
   int32_t group;            /* must be 128 */
   int32_t reserved;         /* must be 0 */
   const uint8_t* codes0;    /* 8-byte aligned */

@@ -29,17 +29,19 @@
 //   s0 * p0 for every (row, half-group) into LDS, the block's records are
 //   processed densely (one per thread) and each adds
 //   mu * sum(x_g) + s1 * sum(t1 * x_g) to its (row, group) slot.
-// * Reduction.  Each row's S partials are summed by one wave: a fixed
-//   strided sum per lane, then an xor butterfly of ds_swizzle steps and a
-//   cross-half readlane.  No atomics: results are bit-identical run to run.
+// * Reduction.  Each row's S partials are summed by one thread in a fixed
+//   order (four accumulators over 16-byte LDS reads; the partial rows are
+//   padded so consecutive threads hit different bank quads).  The two halves
+//   of a group exchange their activation sums with a DPP quad permute.  No
+//   atomics: results are bit-identical run to run.
 
 #include "tq_internal.h"
 
 #ifndef TQ_GEMV_REP
 #define TQ_GEMV_REP 4
 #endif
-#ifndef TQ_GEMV_DEPTH
-#define TQ_GEMV_DEPTH 2
+#ifndef TQ_GEMV_EARLY
+#define TQ_GEMV_EARLY 8
 #endif
 
 namespace tq {
@@ -47,7 +49,9 @@ namespace {
 
 constexpr int kRep = TQ_GEMV_REP;              // LUT copies
 constexpr int kLutBytes = 256 * kRep * 16;
-constexpr int kDepth = TQ_GEMV_DEPTH;          // passes loaded ahead
+// Plane-0 passes issued before the set-up wait; the rest follow the
+// workgroup barrier, so that x and the CSR slice do not queue behind them.
+constexpr int kEarlyMax = TQ_GEMV_EARLY;
 constexpr int kMaxThreads = 1024;
 constexpr int kHalfBytes = 12;                 // body bytes per half-group
 constexpr int kLaneBytes = kHalfBytes + 1;     // + one tail byte
@@ -59,32 +63,29 @@ constexpr int kXStrideDw = 65;
 static_assert(kRep == 1 || kRep == 2 || kRep == 4 || kRep == 8 || kRep == 16, "kRep");
 
 // ---------------------------------------------------------------- table
-struct alignas(16) LutTable {
-  uint32_t v[256][4];
-};
+__device__ inline uint32_t trit_pattern(int t) { return t > 0 ? 0x3C00u : (t < 0 ? 0xBC00u : 0u); }
 
-constexpr uint32_t pattern(int t) { return t > 0 ? 0x3C00u : (t < 0 ? 0xBC00u : 0u); }
-
-constexpr LutTable make_lut() {
-  LutTable L{};
-  for (int c = 0; c < 256; ++c) {
-    uint32_t t[5] = {0, 0, 0, 0, 0};
-    if (c < 243) {
-      int d = c;
-      for (int i = 0; i < 5; ++i) {
-        t[i] = pattern(d % 3 - 1);
-        d /= 3;
-      }
-    }
-    L.v[c][0] = t[0] | (t[1] << 16);
-    L.v[c][1] = t[2] | (t[3] << 16);
-    L.v[c][2] = t[4];
-    L.v[c][3] = 0;
+// Table entry of code c: fp16 patterns of (t0, t1), (t2, t3), (t4, 0);
+// codes 243..255 map to zeros.  Computed in registers (no memory access).
+__device__ inline uint4 lut_entry(int c) {
+  uint32_t t[5];
+  int d = c;
+#pragma unroll
+  for (int i = 0; i < 5; ++i) {
+    t[i] = c < 243 ? trit_pattern(d % 3 - 1) : 0u;
+    d /= 3;
   }
-  return L;
+  return uint4{t[0] | (t[1] << 16), t[2] | (t[3] << 16), t[4], 0u};
 }
 
-__constant__ LutTable kLut = make_lut();
+// Row stride of the LDS partials in floats: at least S, a multiple of 4
+// (16-byte rows), and an odd number of 16-byte slots so that the one-thread-
+// per-row final sum reads different bank quads from consecutive rows.
+__host__ __device__ inline int part_stride(int S) {
+  int ps = ((S + 3) & ~3) + 4;
+  if (((ps >> 2) & 1) == 0) ps += 4;
+  return ps;
+}
 
 // ---------------------------------------------------------------- params
 struct GemvParams {
@@ -110,22 +111,6 @@ __device__ inline float fdot2(uint32_t a, uint32_t b, float c) {
 
 __device__ inline float h2f(uint32_t b) { return (float)__builtin_bit_cast(_Float16, (uint16_t)b); }
 
-template <int Pattern>
-__device__ inline float swz(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), Pattern));
-}
-
-// Sum over the 64 lanes of a wave; every lane returns the same value.
-__device__ inline float wave_sum(float v) {
-  v += swz<0x041F>(v);   // xor 1
-  v += swz<0x081F>(v);   // xor 2
-  v += swz<0x101F>(v);   // xor 4
-  v += swz<0x201F>(v);   // xor 8
-  v += swz<0x401F>(v);   // xor 16
-  const float lo = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
-  const float hi = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
-  return lo + hi;
-}
 
 // LDS byte address of this lane's table copy for byte B of dword w.
 template <int B>
@@ -168,56 +153,57 @@ struct Pass {
   uint32_t sc;     // scale bits
 };
 
-__device__ inline void load_pass(Pass& p, const uint8_t* body, const uint8_t* tail, const uint16_t* scale) {
-  const uint32_t* b = reinterpret_cast<const uint32_t*>(body);
+// Byte offsets fit in 32 bits (the host rejects larger code buffers), so
+// every address is a 64-bit base plus a zero-extended 32-bit offset.
+__device__ inline void load_pass(Pass& p, const uint8_t* body0, const uint8_t* tail0, const uint16_t* scale0,
+                                 uint32_t f) {
+  const uint32_t* b = reinterpret_cast<const uint32_t*>(body0 + (size_t)(kMainBytes * f));
   p.w[0] = __builtin_nontemporal_load(b);
   p.w[1] = __builtin_nontemporal_load(b + 1);
   p.w[2] = __builtin_nontemporal_load(b + 2);
-  p.w[3] = __builtin_nontemporal_load(tail);
-  p.sc = __builtin_nontemporal_load(scale);
+  p.w[3] = __builtin_nontemporal_load(tail0 + (size_t)(2 * f));
+  p.sc = __builtin_nontemporal_load(scale0 + (size_t)f);
 }
 
-// A plane-1 record: 24 body bytes, 2 tail bytes, group, offset, scale.
-struct Rec {
-  uint32_t w[7];
+// Half hh of a plane-1 record: 12 body bytes, its tail byte, and the
+// record's group, offset and scale.
+struct RecHalf {
+  uint32_t w[4];   // w[0..2] body bytes 12 hh .., w[3] tail byte 24 + hh
   uint32_t g, mu, s1;
 };
 
-__device__ inline void load_rec(Rec& r, const MatDev& M, int64_t k) {
-  const uint2* b = reinterpret_cast<const uint2*>(M.codes1 + (int64_t)kMainBytes * k);
-  const uint2 b0 = b[0], b1 = b[1], b2 = b[2];
-  r.w[0] = b0.x; r.w[1] = b0.y; r.w[2] = b1.x; r.w[3] = b1.y; r.w[4] = b2.x; r.w[5] = b2.y;
-  r.w[6] = *reinterpret_cast<const uint16_t*>(M.codes1 + (int64_t)kMainBytes * M.nnz1 + 2 * k);
+__device__ inline void load_rec_half(RecHalf& r, const MatDev& M, uint32_t k, int hh) {
+  const uint32_t* b = reinterpret_cast<const uint32_t*>(M.codes1 + (size_t)(kMainBytes * k + kHalfBytes * hh));
+  r.w[0] = b[0];
+  r.w[1] = b[1];
+  r.w[2] = b[2];
+  r.w[3] = M.codes1[(size_t)(kMainBytes * (uint32_t)M.nnz1 + 2 * k + hh)];
   r.g = M.gidx1[k];
   r.mu = M.offset1[k];
   r.s1 = M.scale1[k];
 }
 
-// mu * sum(x_g) + s1 * sum(t1 x_g) of one record, activations from LDS.
-__device__ __attribute__((always_inline)) inline float record_value(const unsigned char* lut, uint32_t slot,
-                                                                    const uint16_t* xs, const float* gsum,
-                                                                    const Rec& rec, int G) {
-  const int gg = min((int)rec.g, G - 1);
-  float p1 = 0.f;
-#pragma unroll 1
-  for (int hh = 0; hh < 2; ++hh) {
-    const uint32_t hw[4] = {hh ? rec.w[3] : rec.w[0], hh ? rec.w[4] : rec.w[1], hh ? rec.w[5] : rec.w[2],
-                            (rec.w[6] >> (8 * hh)) & 0xFFu};
-    const uint32_t* xd = reinterpret_cast<const uint32_t*>(xs) + kXStrideDw * gg + 30 * hh;   // inputs 60 hh ..
-    const uint16_t* xt = xs + 2 * kXStrideDw * gg + 120 + 5 * hh;
-    p1 += code_dot<kLaneBytes>(lut, slot, hw, [&](int j, int q) -> uint32_t {
-      if (j < kHalfBytes) {
-        const int p = 5 * j + 2 * q;   // input offset within the half
-        if ((p & 1) == 0) return q < 2 ? xd[p / 2] : (xd[p / 2] & 0xFFFFu);
-        return q < 2 ? __builtin_amdgcn_alignbit(xd[(p + 1) / 2], xd[(p - 1) / 2], 16) : (xd[(p - 1) / 2] >> 16);
-      }
-      const int p = 2 * q;             // tail byte: inputs 120 + 5 hh + p
-      const uint32_t a = 120 + 5 * hh + p < kGroup ? (uint32_t)xt[p] : 0u;
-      const uint32_t b = (q < 2 && 121 + 5 * hh + p < kGroup) ? (uint32_t)xt[p + 1] : 0u;
-      return a | (b << 16);
-    });
-  }
-  return h2f(rec.mu) * gsum[gg] + h2f(rec.s1) * p1;
+// Contribution of one record half: s1 * sum(t1 x) over the half, plus
+// mu * sum(x_g) on half 0.  Activations come from LDS.
+__device__ __attribute__((always_inline)) inline float record_half_value(const unsigned char* lut, uint32_t slot,
+                                                                         const uint16_t* xs, const float* gsum,
+                                                                         const RecHalf& r, int hh, int G) {
+  const int gg = min((int)r.g, G - 1);
+  const uint32_t* xd = reinterpret_cast<const uint32_t*>(xs) + kXStrideDw * gg + 30 * hh;   // inputs 60 hh ..
+  const uint16_t* xt = xs + 2 * kXStrideDw * gg + 120 + 5 * hh;
+  const float p1 = code_dot<kLaneBytes>(lut, slot, r.w, [&](int j, int q) -> uint32_t {
+    if (j < kHalfBytes) {
+      const int p = 5 * j + 2 * q;   // input offset within the half
+      if ((p & 1) == 0) return q < 2 ? xd[p / 2] : (xd[p / 2] & 0xFFFFu);
+      return q < 2 ? __builtin_amdgcn_alignbit(xd[(p + 1) / 2], xd[(p - 1) / 2], 16) : (xd[(p - 1) / 2] >> 16);
+    }
+    const int p = 2 * q;             // tail byte: inputs 120 + 5 hh + p
+    const uint32_t a = 120 + 5 * hh + p < kGroup ? (uint32_t)xt[p] : 0u;
+    const uint32_t b = (q < 2 && 121 + 5 * hh + p < kGroup) ? (uint32_t)xt[p + 1] : 0u;
+    return a | (b << 16);
+  });
+  const float v = h2f(r.s1) * p1;
+  return hh == 0 ? h2f(r.mu) * gsum[gg] + v : v;
 }
 
 // kPasses: plane-0 passes per lane, all loaded up front.  kXLoads: 16-byte
@@ -238,7 +224,11 @@ gemv_kernel(const GemvParams P, const uint16_t* __restrict__ x) {
   uint32_t* xsw = reinterpret_cast<uint32_t*>(xs);
   float* gsum = reinterpret_cast<float*>(smem + kLutBytes + 4 * kXStrideDw * G);
   int* rp = reinterpret_cast<int*>(gsum + G);
-  float* part = reinterpret_cast<float*>(rp + P.rb_max + 1);
+  uint16_t* rowof = reinterpret_cast<uint16_t*>(rp + P.rb_max + 1);   // record -> row in block
+  const int rowof_cap = P.rb_max * G;
+  float* part = reinterpret_cast<float*>(
+      (reinterpret_cast<uintptr_t>(rowof + rowof_cap) + 15) & ~static_cast<uintptr_t>(15));
+  const int PS = part_stride(2 * G);
 
   const int tid = threadIdx.x;
   const int T = blockDim.x;
@@ -279,52 +269,78 @@ gemv_kernel(const GemvParams P, const uint16_t* __restrict__ x) {
   const int rp_mine = rpp[has_rec ? min(tid, nrb) : 0];
   const int k0 = rpp[0];
   const int k1 = rpp[has_rec ? nrb : 0];
-  // 2. x and the decode table.
+  // 2. x.
   uint4 xv[kXLoads];
 #pragma unroll
   for (int q = 0; q < kXLoads; ++q) xv[q] = reinterpret_cast<const uint4*>(x)[min(tid + q * T, K / 8 - 1)];
-  const uint4 lutv = *reinterpret_cast<const uint4*>(kLut.v[min(tid, 255)]);
+  // Keep the issue order = the order of need: neither the optimiser nor the
+  // scheduler may move loads across these points (no instruction emitted).
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
   // 3. Every plane-0 pass of this lane.
-  const int64_t ngroups = (int64_t)M.n_out * G;
+  const uint32_t ngroups = (uint32_t)M.n_out * (uint32_t)G;
   const uint8_t* body0 = M.codes0 + kHalfBytes * h;
-  const uint8_t* tail0 = M.codes0 + (int64_t)kMainBytes * ngroups + h;
+  const uint8_t* tail0 = M.codes0 + (size_t)(kMainBytes * ngroups) + h;
+  constexpr int kEarly = kEarlyMax < kPasses ? kEarlyMax : kPasses;
   Pass buf[kPasses];
-#pragma unroll
-  for (int d = 0; d < kPasses; ++d) {
+  auto issue_pass = [&](int d) {
     const int r = min(row_begin + rl + d * ri, row_end - 1);
-    const int64_t f = (int64_t)r * G + g;
-    load_pass(buf[d], body0 + kMainBytes * f, tail0 + 2 * f, M.scale0 + f);
-  }
-  // 4. One record per thread, spread across the waves.
-  const int ri_rec = (tid & 63) * nw + (tid >> 6);
-  const int kr = k0 + ri_rec;
-  const bool rec_valid = has_rec && kr < k1 && kr >= 0 && (int64_t)kr < M.nnz1;
+    load_pass(buf[d], body0, tail0, M.scale0, (uint32_t)r * (uint32_t)G + (uint32_t)g);
+  };
+#pragma unroll
+  for (int d = 0; d < kEarly; ++d) issue_pass(d);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  // 4. Record halves (two threads per record), spread across the waves:
+  //    loaded here when few passes leave registers to spare, else after
+  //    plane 0.
+  constexpr bool kPreRec = kPasses <= 2;
+  const int item = (tid & 63) * nw + (tid >> 6);
+  const int hh = item & 1;
+  const int kr = k0 + (item >> 1);
   MatDev MR = M;
   if (!has_rec) {   // readable stand-ins; the loaded values are ignored
     MR.codes1 = M.codes0;
+    MR.nnz1 = 0;
     MR.gidx1 = MR.offset1 = MR.scale1 = M.scale0;
   }
-  Rec rec;
-  load_rec(rec, MR, rec_valid ? kr : (has_rec ? (int)min((int64_t)max(k0, 0), M.nnz1 - 1) : 0));
+  const int kmax = has_rec ? (int)M.nnz1 - 1 : 0;
+  RecHalf rec;
+  if constexpr (kPreRec) load_rec_half(rec, MR, (uint32_t)min(max(kr, 0), kmax), has_rec ? hh : 0);
 
   // Set-up in LDS.
 #pragma unroll
   for (int q = 0; q < kXLoads; ++q) {
-    const int i = tid + q * T;   // 8 halves: group i / 16, dwords 4 (i % 16) ..
-    if (i < K / 8) {
-      uint32_t* d = xsw + kXStrideDw * (i >> 4) + 4 * (i & 15);
-      d[0] = xv[q].x;
-      d[1] = xv[q].y;
-      d[2] = xv[q].z;
-      d[3] = xv[q].w;
-    }
+    // 8 halves: group i / 16, dwords 4 (i % 16) ..  Unconditional (threads
+    // past the end rewrite the last slot with the same data), so the load is
+    // not sunk into a branch behind the weight loads.
+    const int i = min(tid + q * T, K / 8 - 1);
+    uint32_t* d = xsw + kXStrideDw * (i >> 4) + 4 * (i & 15);
+    d[0] = xv[q].x;
+    d[1] = xv[q].y;
+    d[2] = xv[q].z;
+    d[3] = xv[q].w;
   }
   if (tid < 256) {
+    const uint4 e = lut_entry(tid);
 #pragma unroll
-    for (int q = 0; q < kRep; ++q) reinterpret_cast<uint4*>(lut)[tid * kRep + q] = lutv;
+    for (int q = 0; q < kRep; ++q) reinterpret_cast<uint4*>(lut)[tid * kRep + q] = e;
   }
   if (has_rec && tid <= nrb) rp[tid] = rp_mine;
   __syncthreads();
+  if constexpr (kEarly < kPasses) {
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int d = kEarly; d < kPasses; ++d) issue_pass(d);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // Row of every record of the block (replaces a search per record).
+  if (has_rec && tid < nrb) {
+    const int kb = max(rp[tid], k0), ke = min(rp[tid + 1], k1);
+    for (int k = kb; k < ke && k - k0 < rowof_cap; ++k) rowof[k - k0] = (uint16_t)tid;
+  }
 
   // This lane's activations: 12 body bytes (inputs 60h + 5j ..) and the tail
   // byte (inputs 120 + 5h ..), three fp16 pairs per byte.
@@ -354,14 +370,16 @@ gemv_kernel(const GemvParams P, const uint16_t* __restrict__ x) {
   // Group sums for the offsets: each lane sums its half, the pair combines
   // (half 0 first on both lanes, so both get the same bits).
   {
-    float s = 0.f;
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f;
 #pragma unroll
     for (int j = 0; j < kLaneBytes; ++j) {
-      s = fdot2(xr[j][0], 0x3C003C00u, s);
-      s = fdot2(xr[j][1], 0x3C003C00u, s);
-      s = fdot2(xr[j][2], 0x3C003C00u, s);
+      s0 = fdot2(xr[j][0], 0x3C003C00u, s0);
+      s1 = fdot2(xr[j][1], 0x3C003C00u, s1);
+      s2 = fdot2(xr[j][2], 0x3C003C00u, s2);
     }
-    const float other = swz<0x041F>(s);
+    const float s = (s0 + s1) + s2;
+    const float other = __builtin_bit_cast(   // lane ^ 1 (quad_perm 1,0,3,2)
+        float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, s), 0xB1, 0xF, 0xF, false));
     const float tot = h == 0 ? s + other : other + s;
     if (active && rl == 0 && h == 0) gsum[g] = tot;
   }
@@ -370,69 +388,62 @@ gemv_kernel(const GemvParams P, const uint16_t* __restrict__ x) {
 #pragma unroll
   for (int d = 0; d < kPasses; ++d) {
     const float p = code_dot<kLaneBytes>(lut, slot, buf[d].w, [&](int j, int q) { return xr[j][q]; });
-    if (active && rl + d * ri < nrb) part[(rl + d * ri) * S + sl] = p * h2f(buf[d].sc);
+    if (active && rl + d * ri < nrb) part[(rl + d * ri) * PS + sl] = p * h2f(buf[d].sc);
     __builtin_amdgcn_sched_barrier(0);   // keep passes apart: bounds the LUT reads in flight
   }
   // Plane-0 passes beyond kPasses (only when the host could not fit a
   // matrix into one round of workgroups with kPasses passes).
   for (int d = kPasses; active && rl + d * ri < nrb; ++d) {
-    const int64_t f = (int64_t)(row_begin + rl + d * ri) * G + g;
     Pass q;
-    load_pass(q, body0 + kMainBytes * f, tail0 + 2 * f, M.scale0 + f);
+    load_pass(q, body0, tail0, M.scale0, (uint32_t)(row_begin + rl + d * ri) * (uint32_t)G + (uint32_t)g);
     const float p = code_dot<kLaneBytes>(lut, slot, q.w, [&](int j, int qq) { return xr[j][qq]; });
-    part[(rl + d * ri) * S + sl] = p * h2f(q.sc);
+    part[(rl + d * ri) * PS + sl] = p * h2f(q.sc);
   }
 
-  // Plane 1: each record adds to the (row, group) slot of half 0.
+  // Plane 1: each record half adds to its (row, half-group) slot.
   if (has_rec) {
     __syncthreads();   // plane-0 partials and group sums are in LDS
-    for (int i = ri_rec, k = kr; k0 + i < k1; i += T, k += T) {
-      if (i != ri_rec) load_rec(rec, M, k);
-      if (k < 0 || (int64_t)k >= M.nnz1) break;
-      int lo = 0, hi = nrb - 1;   // last row whose first record is <= k
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (rp[mid] <= k) lo = mid; else hi = mid - 1;
-      }
-      const float v = record_value(lut, slot, xs, gsum, rec, G);
-      float* dst = part + lo * S + 2 * min((int)rec.g, G - 1);
+    const int per_sweep = T >> 1;
+    for (int k = kr, first = 1; k < k1; k += per_sweep, first = 0) {
+      if (!kPreRec || !first) load_rec_half(rec, M, (uint32_t)min(max(k, 0), kmax), hh);
+      if (k < 0 || k - k0 >= rowof_cap) continue;
+      const int lo = min((int)rowof[k - k0], nrb - 1);
+      const float v = record_half_value(lut, slot, xs, gsum, rec, hh, G);
+      float* dst = part + lo * PS + 2 * min((int)rec.g, G - 1) + hh;
       *dst = *dst + v;
     }
   }
   __syncthreads();
 
-  // Row sums: each wave reduces rows wave, wave + nw, ... four at a time.
-  const int lane = tid & 63;
-  for (int r0 = tid >> 6; r0 < nrb; r0 += 4 * nw) {
-    float s[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int rr = r0 + u * nw;
-      s[u] = 0.f;
-      if (rr < nrb)
-        for (int q = lane; q < S; q += 64) s[u] += part[rr * S + q];
+  // Row sums: one thread per row, four independent accumulators over the
+  // row's partials in a fixed order.
+  for (int rr = tid; rr < nrb; rr += T) {
+    const float4* pr = reinterpret_cast<const float4*>(part + rr * PS);
+    float4 a = {0.f, 0.f, 0.f, 0.f};
+    const int n4 = S >> 2;
+    for (int c = 0; c < n4; ++c) {
+      const float4 v = pr[c];
+      a.x += v.x;
+      a.y += v.y;
+      a.z += v.z;
+      a.w += v.w;
     }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) s[u] = wave_sum(s[u]);
-    if (lane == 0) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int rr = r0 + u * nw;
-        if (rr < nrb) {
-          if (P.out_f32)
-            reinterpret_cast<float*>(yp)[row_begin + rr] = s[u];
-          else
-            reinterpret_cast<uint16_t*>(yp)[row_begin + rr] = __builtin_bit_cast(uint16_t, (_Float16)s[u]);
-        }
-      }
+    if (S & 2) {   // S = 2G is even: at most two trailing partials
+      a.x += part[rr * PS + 4 * n4];
+      a.y += part[rr * PS + 4 * n4 + 1];
     }
+    const float sum = (a.x + a.y) + (a.z + a.w);
+    if (P.out_f32)
+      reinterpret_cast<float*>(yp)[row_begin + rr] = sum;
+    else
+      reinterpret_cast<uint16_t*>(yp)[row_begin + rr] = __builtin_bit_cast(uint16_t, (_Float16)sum);
   }
 }
 
 typedef void (*GemvKernel)(const GemvParams, const uint16_t*);
 
-constexpr int kPassChoices[] = {1, 2, 3, 4};
-constexpr int kNumPass = 4;
+constexpr int kPassChoices[] = {1, 2, 3, 4, 6, 8};
+constexpr int kNumPass = 6;
 constexpr int kXChoices[] = {1, 2, 4};
 
 template <int PI, int XI>
@@ -446,6 +457,8 @@ GemvKernel select_kernel(int pi, int xi) {
       {kernel_at<1, 0>(), kernel_at<1, 1>(), kernel_at<1, 2>()},
       {kernel_at<2, 0>(), kernel_at<2, 1>(), kernel_at<2, 2>()},
       {kernel_at<3, 0>(), kernel_at<3, 1>(), kernel_at<3, 2>()},
+      {kernel_at<4, 0>(), kernel_at<4, 1>(), kernel_at<4, 2>()},
+      {kernel_at<5, 0>(), kernel_at<5, 1>(), kernel_at<5, 2>()},
   };
   return table[pi][xi];
 }
@@ -463,8 +476,9 @@ DeviceInfo& device_info() {
 }
 
 size_t lds_bytes(int G, int rb_max) {
-  return (size_t)kLutBytes + 4 * (size_t)kXStrideDw * G + 4 * (size_t)G + 4 * (size_t)(rb_max + 1) +
-         4 * (size_t)rb_max * 2 * G;
+  const size_t head = (size_t)kLutBytes + 4 * (size_t)kXStrideDw * G + 4 * (size_t)G + 4 * (size_t)(rb_max + 1) +
+                      2 * (size_t)rb_max * G;
+  return ((head + 15) & ~(size_t)15) + 4 * (size_t)rb_max * part_stride(2 * G);
 }
 
 }  // namespace
@@ -489,8 +503,8 @@ hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n, const uint16_t*
   // LDS: table + x + group sums + CSR slice + partials.  Two workgroups per
   // CU when they fit in half of the 160 KiB (then at most 512 threads each,
   // 16 waves per CU in all); otherwise one of up to 1024 threads.
-  const size_t fixed = lds_bytes(G, 0);
-  const size_t per_row = 8 * (size_t)G + 4;
+  const size_t fixed = lds_bytes(G, 0) + 16;   // + alignment of the partials
+  const size_t per_row = 4 * (size_t)part_stride(S) + 2 * (size_t)G + 4;
   const size_t half_lds = 80 * 1024, full_lds = 160 * 1024;
   const int ri512 = 512 / S;
   const int wgs_per_cu = (ri512 >= 1 && fixed + per_row * ri512 <= half_lds) ? 2 : 1;

@@ -35,6 +35,8 @@ tq_status check_matrix(const tq_matrix* m, MatDev* d) {
   if (m->n_in < TQ_GROUP || m->n_in % TQ_GROUP != 0) return TQ_ERR_SHAPE;
   const int64_t G = m->n_in / TQ_GROUP;
   if (G > TQ_MAX_GROUPS_PER_ROW) return TQ_ERR_UNSUPPORTED;
+  // Kernels address code buffers with 32-bit byte offsets.
+  if ((int64_t)TQ_GROUP_BYTES * m->n_out * G > (int64_t)UINT32_MAX) return TQ_ERR_UNSUPPORTED;
   if (m->codes0 == nullptr || m->scale0 == nullptr) return TQ_ERR_NULL;
   if (misaligned(m->codes0, 8) || misaligned(m->scale0, 2)) return TQ_ERR_ALIGN;
   if (m->nnz1 < 0 || m->nnz1 > m->n_out * G) return TQ_ERR_SHAPE;
