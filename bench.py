@@ -26,6 +26,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+COPY_BYTES = 256 << 20      # calibration copy: 256 MiB read + 256 MiB written
 
 
 def log(msg):
@@ -75,6 +76,21 @@ def algorithmic_bytes(launches):
         for m in ms:
             total += m.nbytes() + 2 * m.n_in + 2 * m.n_out
     return total
+
+
+def measured_traffic():
+    """HBM bytes per GEMV launch from the committed rocprofv3 summary, if it
+    was taken on the current kernel source (else None)."""
+    import hashlib
+    import re
+    src = os.path.join(ROOT, "paper_2609_09240_amd", "csrc", "gemv.hip")
+    prof = os.path.join(ROOT, "profiles", "gemv_qwen3_8b_decode_step.md")
+    if not os.path.exists(prof):
+        return None
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    m = re.search(r"traffic_bytes_per_launch = (\d+)\s+\(gemv.hip sha256\[:16\] = ([0-9a-f]+)\)",
+                  open(prof).read())
+    return float(m.group(1)) if m and m.group(2) == sha else None
 
 
 def cpu_baseline(layers=2):
@@ -183,6 +199,15 @@ def main():
     bytes_per_launch = step_bytes / len(launches)
     achieved = bytes_per_launch / (avg_ms * 1e-3) / 1e9
 
+    # Calibration for HBM counters: a plain copy of known size (outside the
+    # timed region), so FETCH_SIZE / WRITE_SIZE of the GEMV can be scaled.
+    cal = torch.empty(COPY_BYTES // 2, dtype=torch.float16, device=dev)
+    cal_dst = torch.empty_like(cal)
+    for _ in range(3):
+        cal_dst.copy_(cal)
+    torch.cuda.synchronize()
+    del cal, cal_dst
+
     result = {
         "metric": "packed ternary GEMV HBM GB/s (% of peak) + us per Qwen3-8B decode-step linears",
         "value": round(gbs, 2),
@@ -216,7 +241,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(),
             "avg_launch_us": round(avg_ms * 1e3, 3),
             "bytes_per_launch": round(bytes_per_launch, 1),
         },

@@ -306,7 +306,10 @@ gemv_kernel(const GemvParams P, const uint16_t* __restrict__ x) {
   }
   const int kmax = has_rec ? (int)M.nnz1 - 1 : 0;
   RecHalf rec;
-  if constexpr (kPreRec) load_rec_half(rec, MR, (uint32_t)min(max(kr, 0), kmax), has_rec ? hh : 0);
+  // Threads past the block's records reload its last record (no extra
+  // cache lines); the values are ignored.
+  const int k_last = min(max(k1 - 1, k0), kmax);
+  if constexpr (kPreRec) load_rec_half(rec, MR, (uint32_t)max(min(kr, k_last), 0), has_rec ? hh : 0);
 
   // Set-up in LDS.
 #pragma unroll
