@@ -24,6 +24,9 @@ FLAGS = [
     "-Wall",
     # Packed fp32 VALU forms stay disabled in all device code.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # The first 14 argument dwords arrive in SGPRs at wave start (the GEMV
+    # finds its matrix from them without a memory round trip).
+    "-mllvm", "-amdgpu-kernarg-preload-count=14",
     "-I" + os.path.join(ROOT, "include"),
 ]
 

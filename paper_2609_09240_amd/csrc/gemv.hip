@@ -88,16 +88,26 @@ __host__ __device__ inline int part_stride(int S) {
 }
 
 // ---------------------------------------------------------------- params
-struct GemvParams {
-  MatDev m[TQ_MAX_GROUPED];
-  void* y[TQ_MAX_GROUPED];
-  int32_t wg_begin[TQ_MAX_GROUPED + 1];
-  int32_t rows_per_wg;
-  int32_t n_mats;
-  int32_t G;        // groups per row, shared by all matrices
-  int32_t ri;       // rows per pass = T / (2G)
-  int32_t rb_max;   // rows per LDS block
-  int32_t out_f32;
+// Per-matrix launch record.  The kernel reads the one its workgroup serves
+// straight from the kernel-argument segment (one scalar memory round trip);
+// everything needed to find it is in the leading scalar arguments, which the
+// build asks the hardware to preload into SGPRs.
+struct GemvMat {
+  const uint8_t* codes0;
+  const uint16_t* scale0;
+  const int32_t* rowptr1;
+  const uint16_t* gidx1;
+  const uint8_t* codes1;
+  const uint16_t* offset1;
+  const uint16_t* scale1;
+  void* y;
+  int32_t n_out;
+  int32_t nnz1;       // < 2^31: the host caps code buffers at 2^32 bytes
+  int32_t wg_begin;   // first workgroup of this matrix
+  int32_t pad;
+};
+struct GemvMats {
+  GemvMat m[TQ_MAX_GROUPED];
 };
 
 struct __attribute__((aligned(16))) U3 {
@@ -172,12 +182,21 @@ struct RecHalf {
   uint32_t g, mu, s1;
 };
 
-__device__ inline void load_rec_half(RecHalf& r, const MatDev& M, uint32_t k, int hh) {
+// Where a workgroup reads its records from.
+struct RecSrc {
+  const uint8_t* codes1;
+  const uint16_t* gidx1;
+  const uint16_t* offset1;
+  const uint16_t* scale1;
+  uint32_t nnz1;
+};
+
+__device__ inline void load_rec_half(RecHalf& r, const RecSrc& M, uint32_t k, int hh) {
   const uint32_t* b = reinterpret_cast<const uint32_t*>(M.codes1 + (size_t)(kMainBytes * k + kHalfBytes * hh));
   r.w[0] = b[0];
   r.w[1] = b[1];
   r.w[2] = b[2];
-  r.w[3] = M.codes1[(size_t)(kMainBytes * (uint32_t)M.nnz1 + 2 * k + hh)];
+  r.w[3] = M.codes1[(size_t)(kMainBytes * M.nnz1 + 2 * k + hh)];
   r.g = M.gidx1[k];
   r.mu = M.offset1[k];
   r.s1 = M.scale1[k];
@@ -214,9 +233,10 @@ __device__ __attribute__((always_inline)) inline float record_half_value(const u
 // bytes stream in behind it.
 template <int kPasses, int kXLoads>
 __global__ void __launch_bounds__(kMaxThreads) __attribute__((amdgpu_waves_per_eu(4)))
-gemv_kernel(const GemvParams P, const uint16_t* __restrict__ x) {
+gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_per_wg, int32_t out_f32,
+            int32_t wb1, int32_t wb2, int32_t wb3, int32_t wb4, int32_t wb5, int32_t wb6, int32_t wb7,
+            int32_t nthreads, const GemvMats mats) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  const int G = P.G;
   const int S = 2 * G;
   const int K = G * kGroup;
   unsigned char* lut = smem;
@@ -224,37 +244,34 @@ gemv_kernel(const GemvParams P, const uint16_t* __restrict__ x) {
   uint32_t* xsw = reinterpret_cast<uint32_t*>(xs);
   float* gsum = reinterpret_cast<float*>(smem + kLutBytes + 4 * kXStrideDw * G);
   int* rp = reinterpret_cast<int*>(gsum + G);
-  uint16_t* rowof = reinterpret_cast<uint16_t*>(rp + P.rb_max + 1);   // record -> row in block
-  const int rowof_cap = P.rb_max * G;
+  uint16_t* rowof = reinterpret_cast<uint16_t*>(rp + rows_per_wg + 1);   // record -> row in block
+  const int rowof_cap = rows_per_wg * G;
   float* part = reinterpret_cast<float*>(
       (reinterpret_cast<uintptr_t>(rowof + rowof_cap) + 15) & ~static_cast<uintptr_t>(15));
   const int PS = part_stride(2 * G);
 
   const int tid = threadIdx.x;
-  const int T = blockDim.x;
+  const int T = nthreads;   // == blockDim.x, without a load of the dispatch packet
   const int nw = T >> 6;
 
-  // Which matrix this workgroup serves (constant indices only, so the
-  // parameter block is never copied to scratch).
-  int mi = 0;
-#pragma unroll
-  for (int i = 1; i < TQ_MAX_GROUPED; ++i)
-    if (i < P.n_mats && (int)blockIdx.x >= P.wg_begin[i]) mi = i;
-  MatDev M = P.m[0];
-  void* yp = P.y[0];
-  int wgb = P.wg_begin[0];
-#pragma unroll
-  for (int i = 1; i < TQ_MAX_GROUPED; ++i)
-    if (i == mi) {
-      M = P.m[i];
-      yp = P.y[i];
-      wgb = P.wg_begin[i];
-    }
-  const int row_begin = ((int)blockIdx.x - wgb) * P.rows_per_wg;
-  const int row_end = min(M.n_out, row_begin + P.rows_per_wg);
+  // Which matrix this workgroup serves: the first workgroups of matrices
+  // 1..7 arrive in SGPRs (unused ones are INT32_MAX), so the matrix record
+  // is one scalar load away.
+  const int w = blockIdx.x;
+  const int sel = __builtin_amdgcn_readfirstlane((w >= wb1) + (w >= wb2) + (w >= wb3) + (w >= wb4) + (w >= wb5) +
+                                                 (w >= wb6) + (w >= wb7));
+  // The whole record in one batch of scalar loads and one wait (left to
+  // itself the compiler fetches fields at their first use, one round trip
+  // each).
+  const GemvMat M = mats.m[sel];
+  asm volatile("" ::"s"(M.codes0), "s"(M.scale0), "s"(M.rowptr1), "s"(M.gidx1), "s"(M.codes1), "s"(M.offset1),
+               "s"(M.scale1), "s"(M.y), "s"(M.n_out), "s"(M.nnz1), "s"(M.wg_begin));
+  __builtin_amdgcn_sched_barrier(0);
+  void* const yp = M.y;
+  const int row_begin = (w - M.wg_begin) * rows_per_wg;
+  const int row_end = min(M.n_out, row_begin + rows_per_wg);
   const int nrb = row_end - row_begin;
 
-  const int ri = P.ri;
   const bool active = tid < ri * S;
   const int sl = active ? tid % S : 0;   // half-group slot within the row
   const int g = sl >> 1;
@@ -298,13 +315,15 @@ gemv_kernel(const GemvParams P, const uint16_t* __restrict__ x) {
   const int item = (tid & 63) * nw + (tid >> 6);
   const int hh = item & 1;
   const int kr = k0 + (item >> 1);
-  MatDev MR = M;
-  if (!has_rec) {   // readable stand-ins; the loaded values are ignored
-    MR.codes1 = M.codes0;
-    MR.nnz1 = 0;
-    MR.gidx1 = MR.offset1 = MR.scale1 = M.scale0;
-  }
-  const int kmax = has_rec ? (int)M.nnz1 - 1 : 0;
+  // Without records, plane-0 arrays stand in as readable addresses (the
+  // loaded values are ignored).
+  RecSrc MR;
+  MR.codes1 = has_rec ? M.codes1 : M.codes0;
+  MR.nnz1 = has_rec ? (uint32_t)M.nnz1 : 0u;
+  MR.gidx1 = has_rec ? M.gidx1 : M.scale0;
+  MR.offset1 = has_rec ? M.offset1 : M.scale0;
+  MR.scale1 = has_rec ? M.scale1 : M.scale0;
+  const int kmax = has_rec ? M.nnz1 - 1 : 0;
   RecHalf rec;
   // Threads past the block's records reload its last record (no extra
   // cache lines); the values are ignored.
@@ -408,7 +427,7 @@ gemv_kernel(const GemvParams P, const uint16_t* __restrict__ x) {
     __syncthreads();   // plane-0 partials and group sums are in LDS
     const int per_sweep = T >> 1;
     for (int k = kr, first = 1; k < k1; k += per_sweep, first = 0) {
-      if (!kPreRec || !first) load_rec_half(rec, M, (uint32_t)min(max(k, 0), kmax), hh);
+      if (!kPreRec || !first) load_rec_half(rec, MR, (uint32_t)min(max(k, 0), kmax), hh);
       if (k < 0 || k - k0 >= rowof_cap) continue;
       const int lo = min((int)rowof[k - k0], nrb - 1);
       const float v = record_half_value(lut, slot, xs, gsum, rec, hh, G);
@@ -436,14 +455,15 @@ gemv_kernel(const GemvParams P, const uint16_t* __restrict__ x) {
       a.y += part[rr * PS + 4 * n4 + 1];
     }
     const float sum = (a.x + a.y) + (a.z + a.w);
-    if (P.out_f32)
+    if (out_f32)
       reinterpret_cast<float*>(yp)[row_begin + rr] = sum;
     else
       reinterpret_cast<uint16_t*>(yp)[row_begin + rr] = __builtin_bit_cast(uint16_t, (_Float16)sum);
   }
 }
 
-typedef void (*GemvKernel)(const GemvParams, const uint16_t*);
+typedef void (*GemvKernel)(const uint16_t*, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t,
+                           int32_t, int32_t, int32_t, int32_t, const GemvMats);
 
 constexpr int kPassChoices[] = {1, 2, 3, 4, 6, 8};
 constexpr int kNumPass = 6;
@@ -497,7 +517,6 @@ hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n, const uint16_t*
     if (e != hipSuccess) return e;
   }
 
-  GemvParams P = {};
   const int G = ms[0].n_groups;
   const int S = 2 * G;
   int64_t total_rows = 0;
@@ -555,21 +574,29 @@ hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n, const uint16_t*
     di.attr_set[pi][xi] = true;
   }
 
+  GemvMats A = {};
+  int32_t wb[TQ_MAX_GROUPED];
   int wg = 0;
-  for (int i = 0; i < n; ++i) {
-    P.m[i] = ms[i];
-    P.y[i] = ys[i];
-    P.wg_begin[i] = wg;
+  for (int i = 0; i < TQ_MAX_GROUPED; ++i) {
+    wb[i] = INT32_MAX;
+    if (i >= n) continue;
+    GemvMat& a = A.m[i];
+    a.codes0 = ms[i].codes0;
+    a.scale0 = ms[i].scale0;
+    a.rowptr1 = ms[i].rowptr1;
+    a.gidx1 = ms[i].gidx1;
+    a.codes1 = ms[i].codes1;
+    a.offset1 = ms[i].offset1;
+    a.scale1 = ms[i].scale1;
+    a.y = ys[i];
+    a.n_out = ms[i].n_out;
+    a.nnz1 = (int32_t)ms[i].nnz1;
+    a.wg_begin = wg;
+    wb[i] = wg;
     wg += (ms[i].n_out + rows_per_wg - 1) / rows_per_wg;
   }
-  P.wg_begin[n] = wg;
-  P.rows_per_wg = rows_per_wg;
-  P.n_mats = n;
-  P.G = G;
-  P.ri = ri;
-  P.rb_max = rows_per_wg;
-  P.out_f32 = out_f32 ? 1 : 0;
-  hipLaunchKernelGGL(kern, dim3(wg), dim3(T), lds_bytes(G, rows_per_wg), s, P, x);
+  hipLaunchKernelGGL(kern, dim3(wg), dim3(T), lds_bytes(G, rows_per_wg), s, x, G, ri, rows_per_wg,
+                     out_f32 ? 1 : 0, wb[1], wb[2], wb[3], wb[4], wb[5], wb[6], wb[7], T, A);
   return hipGetLastError();
 }
 
