@@ -65,7 +65,7 @@
 extern "C" {
 #endif
 
-#define TQ_ABI_VERSION 1
+#define TQ_ABI_VERSION 2
 #define TQ_GROUP 128
 #define TQ_GROUP_BYTES 26
 #define TQ_MAX_GROUPS_PER_ROW 256    /* K <= 32768 */
@@ -102,6 +102,12 @@ typedef struct tq_matrix {
   const uint8_t* codes1;    /* 8-byte aligned */
   const uint16_t* offset1;
   const uint16_t* scale1;
+  /* Optional (may be NULL): a HOST copy of rowptr1, read during the call
+   * only.  With it the GEMV finds every workgroup's records on the host and
+   * issues their loads with its first batch, instead of reading the device
+   * row pointers first.  It must hold the same values as rowptr1; if it does
+   * not, results are unspecified, but every access stays in bounds. */
+  const int32_t* rowptr1_host;
 } tq_matrix;
 
 /* Version of this ABI (TQ_ABI_VERSION). */

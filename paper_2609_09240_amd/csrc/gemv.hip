@@ -8,50 +8,50 @@
 //
 // * Lane ownership.  A row of G groups is split into S = 2G half-groups: half
 //   h of group g holds code bytes 12h .. 12h+11 (inputs 60h .. 60h+59) plus
-//   tail byte 24+h (inputs 120+5h ..).  A workgroup of T threads covers
-//   RI = T / S rows per pass and thread t always owns half-group t % S, so its
-//   activations stay in 39 VGPRs for the whole launch, laid out per code byte
-//   j as the fp16 pairs (x5j, x5j+1), (x5j+2, x5j+3), (x5j+4, 0).
+//   tail byte 24+h (inputs 120+5h ..).  Rows are laid on SP lanes, SP = S
+//   rounded up to a divisor or a multiple of 64, so that no row straddles a
+//   wave boundary; a workgroup of T threads covers RI = T / SP rows per pass
+//   and thread t always owns half-group t % SP, so its activations stay in 39
+//   VGPRs for the whole launch, laid out per code byte j as the fp16 pairs
+//   (x5j, x5j+1), (x5j+2, x5j+3), (x5j+4, 0).
 // * Decode.  A 256-entry table maps a code to the same three pairs of fp16
 //   patterns (+1 = 0x3C00, -1 = 0xBC00, 0 = 0); three v_dot2_f32_f16 then
 //   accumulate the sign-selected activations in fp32.  The table is
-//   replicated kRep times in LDS (copy q of code c at byte 16 (kRep c + q)); a
-//   lane reads copy lane % kRep, so lanes served in the same LDS cycle hit
-//   different bank quads whatever codes they hold.  With kRep = 16 the table
-//   address (c << 8) | 16 q is one v_perm_b32 of the code dword.
+//   replicated kRep = 16 times in LDS (copy q of code c at byte 16 (16 c + q),
+//   64 KiB); a lane reads copy lane % 16 (12 bytes), so lanes read together
+//   sit on different banks whatever codes they hold (four copies cost two to
+//   three times as many LDS cycles in bank conflicts).
 // * Loads.  Per pass a lane loads 12 body bytes (three dwords, 4-aligned in
 //   the split layout), its tail byte and its group's scale; lanes of a row
-//   read consecutive bytes, so every wave load is contiguous.  Loads run
-//   kDepth passes ahead of the decode (register ring), and each thread's
-//   first plane-1 record is loaded before the workgroup's set-up, so HBM
-//   latency overlaps the set-up and the plane-0 pass.
-// * Plane 1.  After the plane-0 pass over a block of rows has written
-//   s0 * p0 for every (row, half-group) into LDS, the block's records are
-//   processed densely (one per thread) and each adds
-//   mu * sum(x_g) + s1 * sum(t1 * x_g) to its (row, group) slot.
-// * Reduction.  Each row's S partials are summed by one thread in a fixed
-//   order (four accumulators over 16-byte LDS reads; the partial rows are
-//   padded so consecutive threads hit different bank quads).  The two halves
-//   of a group exchange their activation sums with a DPP quad permute.  No
-//   atomics: results are bit-identical run to run.
+//   read consecutive bytes, so every wave load is contiguous.  All loads of a
+//   workgroup are issued before its first wait, in the order their data is
+//   needed, and every one is unconditional (clamped addresses), so each wait
+//   is an exact vmcnt.  The matrix record is read from the kernel-argument
+//   segment with one scalar round trip; the leading arguments that select it
+//   are preloaded into SGPRs.
+// * Plane 1.  Each record is handled by two threads (one per half).  A
+//   record half adds s1 * sum(t1 x) + mu * sum(x) over its half-group into a
+//   per-(row, half-group) LDS slot; the slot array starts at zero.  Records
+//   are handled after plane 0.  When the host passes each workgroup's record
+//   range, their loads go out with the first batch; otherwise the range
+//   needs the row pointers first (one more memory round trip).
+// * Reduction.  Plane-0 partials stay in registers; each lane adds its
+//   record slot and the row is summed across its lanes with DPP butterflies
+//   (every lane of a row ends with the same bits), plus one LDS step when a
+//   row spans several waves.  No atomics: results are bit-identical run to
+//   run.
 
 #include "tq_internal.h"
 
-#ifndef TQ_GEMV_REP
-#define TQ_GEMV_REP 4
-#endif
-#ifndef TQ_GEMV_EARLY
-#define TQ_GEMV_EARLY 8
-#endif
+// Products and sums are rounded as written (no fused multiply-add), so the
+// result does not depend on which of the kernel variants runs.
+#pragma clang fp contract(off)
 
 namespace tq {
 namespace {
 
-constexpr int kRep = TQ_GEMV_REP;              // LUT copies
+constexpr int kRep = 16;                       // LUT copies
 constexpr int kLutBytes = 256 * kRep * 16;
-// Plane-0 passes issued before the set-up wait; the rest follow the
-// workgroup barrier, so that x and the CSR slice do not queue behind them.
-constexpr int kEarlyMax = TQ_GEMV_EARLY;
 constexpr int kMaxThreads = 1024;
 constexpr int kHalfBytes = 12;                 // body bytes per half-group
 constexpr int kLaneBytes = kHalfBytes + 1;     // + one tail byte
@@ -59,8 +59,22 @@ constexpr int kLaneBytes = kHalfBytes + 1;     // + one tail byte
 // the 64 lanes of a wave (32 groups x 2 halves) on different banks when they
 // read their activations.
 constexpr int kXStrideDw = 65;
+// Record-range table entries passed with a launch (host ranges).
+constexpr int kMaxRangeEntries = 768;
 
-static_assert(kRep == 1 || kRep == 2 || kRep == 4 || kRep == 8 || kRep == 16, "kRep");
+static_assert(kRep == 16, "the table addressing assumes 16 copies");
+
+// Lanes per row: S itself when it is a multiple of 64, else S rounded up to
+// a power of two (S < 64) or to a multiple of 64 (S > 64).
+__host__ __device__ inline int padded_slots(int S) {
+  if ((S & 63) == 0) return S;
+  if (S < 64) {
+    int p = 2;
+    while (p < S) p <<= 1;
+    return p;
+  }
+  return (S + 63) & ~63;
+}
 
 // ---------------------------------------------------------------- table
 __device__ inline uint32_t trit_pattern(int t) { return t > 0 ? 0x3C00u : (t < 0 ? 0xBC00u : 0u); }
@@ -69,29 +83,19 @@ __device__ inline uint32_t trit_pattern(int t) { return t > 0 ? 0x3C00u : (t < 0
 // codes 243..255 map to zeros.  Computed in registers (no memory access).
 __device__ inline uint4 lut_entry(int c) {
   uint32_t t[5];
-  int d = c;
+  uint32_t d = (uint32_t)c;
 #pragma unroll
   for (int i = 0; i < 5; ++i) {
-    t[i] = c < 243 ? trit_pattern(d % 3 - 1) : 0u;
-    d /= 3;
+    const uint32_t q = (d * 171u) >> 9;   // d / 3 for d < 256
+    t[i] = c < 243 ? trit_pattern((int)(d - 3u * q) - 1) : 0u;
+    d = q;
   }
   return uint4{t[0] | (t[1] << 16), t[2] | (t[3] << 16), t[4], 0u};
 }
 
-// Row stride of the LDS partials in floats: at least S, a multiple of 4
-// (16-byte rows), and an odd number of 16-byte slots so that the one-thread-
-// per-row final sum reads different bank quads from consecutive rows.
-__host__ __device__ inline int part_stride(int S) {
-  int ps = ((S + 3) & ~3) + 4;
-  if (((ps >> 2) & 1) == 0) ps += 4;
-  return ps;
-}
-
 // ---------------------------------------------------------------- params
-// Per-matrix launch record.  The kernel reads the one its workgroup serves
-// straight from the kernel-argument segment (one scalar memory round trip);
-// everything needed to find it is in the leading scalar arguments, which the
-// build asks the hardware to preload into SGPRs.
+// Per-matrix launch record, read by the kernel straight from the kernel-
+// argument segment.
 struct GemvMat {
   const uint8_t* codes0;
   const uint16_t* scale0;
@@ -106,9 +110,14 @@ struct GemvMat {
   int32_t wg_begin;   // first workgroup of this matrix
   int32_t pad;
 };
-struct GemvMats {
+struct GemvArgs {
   GemvMat m[TQ_MAX_GROUPED];
+  // With host ranges: the first record of every workgroup, matrix by
+  // matrix, each matrix closed by its nnz1 (entry of workgroup w of matrix
+  // i is rec_begin[w + i]).
+  int32_t rec_begin[kMaxRangeEntries];
 };
+
 
 struct __attribute__((aligned(16))) U3 {
   uint32_t x, y, z;
@@ -121,27 +130,21 @@ __device__ inline float fdot2(uint32_t a, uint32_t b, float c) {
 
 __device__ inline float h2f(uint32_t b) { return (float)__builtin_bit_cast(_Float16, (uint16_t)b); }
 
-
 // LDS byte address of this lane's table copy for byte B of dword w.
 template <int B>
 __device__ inline uint32_t lut_addr(uint32_t w, uint32_t slot) {
-  if constexpr (kRep == 16) {
-    // bytes [slot, code, 0, 0]: selector 4 picks byte 0 of `slot`, B byte B of w.
-    return __builtin_amdgcn_perm(slot, w, 0x0C0C0004u | (B << 8));
-  } else {
-    constexpr int sh = 4 + (kRep == 8 ? 3 : kRep == 4 ? 2 : kRep == 2 ? 1 : 0);
-    return (((w >> (8 * B)) & 0xFFu) << sh) | slot;
-  }
+  // bytes [slot, code, 0, 0]: selector 4 picks byte 0 of `slot`, B byte B of w.
+  return __builtin_amdgcn_perm(slot, w, 0x0C0C0004u | (B << 8));
 }
 
-// Dot product of NB code bytes (byte j in byte j % 4 of w[j / 4]) with the
-// activation pairs xp(j, q).
-template <int NB, typename W, typename XP>
+// Dot product of the 13 code bytes of a half-group (byte j in byte j % 4 of
+// w[j / 4]) with activation pairs xr[j][q].
 __device__ __attribute__((always_inline)) inline float code_dot(const unsigned char* lut, uint32_t slot,
-                                                                const W& w, XP xp) {
+                                                                const uint32_t (&w)[4],
+                                                                const uint32_t (&xr)[kLaneBytes][3]) {
   float a0 = 0.f, a1 = 0.f, a2 = 0.f;
 #pragma unroll
-  for (int j = 0; j < NB; ++j) {
+  for (int j = 0; j < kLaneBytes; ++j) {
     uint32_t addr;
     switch (j & 3) {
       case 0: addr = lut_addr<0>(w[j >> 2], slot); break;
@@ -150,11 +153,37 @@ __device__ __attribute__((always_inline)) inline float code_dot(const unsigned c
       default: addr = lut_addr<3>(w[j >> 2], slot); break;
     }
     const U3 p = *reinterpret_cast<const U3*>(lut + addr);
-    a0 = fdot2(p.x, xp(j, 0), a0);
-    a1 = fdot2(p.y, xp(j, 1), a1);
-    a2 = fdot2(p.z, xp(j, 2), a2);
+    a0 = fdot2(p.x, xr[j][0], a0);
+    a1 = fdot2(p.y, xr[j][1], a1);
+    a2 = fdot2(p.z, xr[j][2], a2);
   }
   return (a0 + a1) + a2;
+}
+
+// Activations of half h of group g from the LDS copy of x: 12 body bytes
+// (inputs 60h + 5j ..) and the tail byte (inputs 120 + 5h ..), three fp16
+// pairs per byte; inputs past the group (pad digits) are zero.
+__device__ __attribute__((always_inline)) inline void load_xr(uint32_t (&xr)[kLaneBytes][3], const uint32_t* xsw,
+                                                              int g, int h) {
+  const uint32_t* xd = xsw + kXStrideDw * g + 30 * h;   // inputs 60 h ..
+#pragma unroll
+  for (int j = 0; j < kHalfBytes; j += 2) {   // bytes j, j+1: inputs 5j .. 5j+9 = dwords 5j/2 ..
+    const int q = 5 * j / 2;
+    const uint32_t d0 = xd[q], d1 = xd[q + 1], d2 = xd[q + 2], d3 = xd[q + 3], d4 = xd[q + 4];
+    xr[j][0] = d0;
+    xr[j][1] = d1;
+    xr[j][2] = d2 & 0xFFFFu;
+    xr[j + 1][0] = __builtin_amdgcn_alignbit(d3, d2, 16);
+    xr[j + 1][1] = __builtin_amdgcn_alignbit(d4, d3, 16);
+    xr[j + 1][2] = d4 >> 16;
+  }
+  const uint16_t* xt = reinterpret_cast<const uint16_t*>(xsw + kXStrideDw * g) + 120 + 5 * h;
+  uint32_t e[5];
+#pragma unroll
+  for (int i = 0; i < 5; ++i) e[i] = (120 + 5 * h + i < kGroup) ? (uint32_t)xt[i] : 0u;
+  xr[kHalfBytes][0] = e[0] | (e[1] << 16);
+  xr[kHalfBytes][1] = e[2] | (e[3] << 16);
+  xr[kHalfBytes][2] = e[4];
 }
 
 // One pass of plane 0 for one lane: 12 body bytes, 1 tail byte, 1 scale.
@@ -175,13 +204,6 @@ __device__ inline void load_pass(Pass& p, const uint8_t* body0, const uint8_t* t
   p.sc = __builtin_nontemporal_load(scale0 + (size_t)f);
 }
 
-// Half hh of a plane-1 record: 12 body bytes, its tail byte, and the
-// record's group, offset and scale.
-struct RecHalf {
-  uint32_t w[4];   // w[0..2] body bytes 12 hh .., w[3] tail byte 24 + hh
-  uint32_t g, mu, s1;
-};
-
 // Where a workgroup reads its records from.
 struct RecSrc {
   const uint8_t* codes1;
@@ -189,6 +211,13 @@ struct RecSrc {
   const uint16_t* offset1;
   const uint16_t* scale1;
   uint32_t nnz1;
+};
+
+// Half hh of a plane-1 record: 12 body bytes, its tail byte, and the
+// record's group, offset and scale.
+struct RecHalf {
+  uint32_t w[4];   // w[0..2] body bytes 12 hh .., w[3] tail byte 24 + hh
+  uint32_t g, mu, s1;
 };
 
 __device__ inline void load_rec_half(RecHalf& r, const RecSrc& M, uint32_t k, int hh) {
@@ -202,57 +231,87 @@ __device__ inline void load_rec_half(RecHalf& r, const RecSrc& M, uint32_t k, in
   r.s1 = M.scale1[k];
 }
 
-// Contribution of one record half: s1 * sum(t1 x) over the half, plus
-// mu * sum(x_g) on half 0.  Activations come from LDS.
+// Contribution of one record half: s1 * sum(t1 x) + mu * sum(x) over the
+// half-group (the two halves together give mu * sum(x_g) + s1 * sum(t1 x_g)).
 __device__ __attribute__((always_inline)) inline float record_half_value(const unsigned char* lut, uint32_t slot,
-                                                                         const uint16_t* xs, const float* gsum,
-                                                                         const RecHalf& r, int hh, int G) {
-  const int gg = min((int)r.g, G - 1);
-  const uint32_t* xd = reinterpret_cast<const uint32_t*>(xs) + kXStrideDw * gg + 30 * hh;   // inputs 60 hh ..
-  const uint16_t* xt = xs + 2 * kXStrideDw * gg + 120 + 5 * hh;
-  const float p1 = code_dot<kLaneBytes>(lut, slot, r.w, [&](int j, int q) -> uint32_t {
-    if (j < kHalfBytes) {
-      const int p = 5 * j + 2 * q;   // input offset within the half
-      if ((p & 1) == 0) return q < 2 ? xd[p / 2] : (xd[p / 2] & 0xFFFFu);
-      return q < 2 ? __builtin_amdgcn_alignbit(xd[(p + 1) / 2], xd[(p - 1) / 2], 16) : (xd[(p - 1) / 2] >> 16);
+                                                                         const uint32_t* xsw, const RecHalf& r,
+                                                                         int hh, int G) {
+  uint32_t xr[kLaneBytes][3];
+  load_xr(xr, xsw, min((int)r.g, G - 1), hh);
+  float s0 = 0.f, s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int j = 0; j < kLaneBytes; ++j) {
+    s0 = fdot2(xr[j][0], 0x3C003C00u, s0);
+    s1 = fdot2(xr[j][1], 0x3C003C00u, s1);
+    s2 = fdot2(xr[j][2], 0x3C003C00u, s2);
+  }
+  const float xsum = (s0 + s1) + s2;
+  const float p1 = code_dot(lut, slot, r.w, xr);
+  return h2f(r.s1) * p1 + h2f(r.mu) * xsum;
+}
+
+// Sum of v over aligned segments of seg lanes (seg a power of two <= 64);
+// every lane of a segment returns the same bits.
+__device__ __attribute__((always_inline)) inline float segment_sum(float v, int seg) {
+  auto dpp = [](float a, int ctrl) -> float {
+    int r;
+    switch (ctrl) {
+      case 0: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, a), 0xB1, 0xF, 0xF, false); break;    // xor 1
+      case 1: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, a), 0x4E, 0xF, 0xF, false); break;    // xor 2
+      case 2: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, a), 0x141, 0xF, 0xF, false); break;   // half-row mirror
+      default: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, a), 0x140, 0xF, 0xF, false); break;  // row mirror
     }
-    const int p = 2 * q;             // tail byte: inputs 120 + 5 hh + p
-    const uint32_t a = 120 + 5 * hh + p < kGroup ? (uint32_t)xt[p] : 0u;
-    const uint32_t b = (q < 2 && 121 + 5 * hh + p < kGroup) ? (uint32_t)xt[p + 1] : 0u;
-    return a | (b << 16);
-  });
-  const float v = h2f(r.s1) * p1;
-  return hh == 0 ? h2f(r.mu) * gsum[gg] + v : v;
+    return __builtin_bit_cast(float, r);
+  };
+  if (seg >= 2) v = v + dpp(v, 0);
+  if (seg >= 4) v = v + dpp(v, 1);
+  if (seg >= 8) v = v + dpp(v, 2);
+  if (seg >= 16) v = v + dpp(v, 3);
+  if (seg >= 32) {
+    const int lane = __lane_id();
+    const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+    const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+    const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+    const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+    const float lo = r0 + r1, hi = r2 + r3;
+    v = seg == 64 ? lo + hi : (lane < 32 ? lo : hi);
+  }
+  return v;
+}
+
+__device__ inline void store_y(void* y, int i, float v, int out_f32) {
+  if (out_f32)
+    reinterpret_cast<float*>(y)[i] = v;
+  else
+    reinterpret_cast<uint16_t*>(y)[i] = __builtin_bit_cast(uint16_t, (_Float16)v);
 }
 
 // kPasses: plane-0 passes per lane, all loaded up front.  kXLoads: 16-byte
-// loads of x per thread (ceil(K / 8 / T)).  Every global load of the
-// preamble is unconditional (out-of-range lanes load a valid address and
-// ignore it) and issued in the order the data is needed, so each wait is an
-// exact vmcnt and one memory round trip covers the set-up while the plane-0
-// bytes stream in behind it.
-template <int kPasses, int kXLoads>
+// loads of x per thread (ceil(K / 8 / T)).  kHostRanges: the host passes
+// each workgroup's record range.
+template <int kPasses, int kXLoads, bool kHostRanges>
 __global__ void __launch_bounds__(kMaxThreads) __attribute__((amdgpu_waves_per_eu(4)))
 gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_per_wg, int32_t out_f32,
             int32_t wb1, int32_t wb2, int32_t wb3, int32_t wb4, int32_t wb5, int32_t wb6, int32_t wb7,
-            int32_t nthreads, const GemvMats mats) {
+            int32_t nthreads, const GemvArgs args) {
+  // The table is the kernel's only static LDS, so it sits at LDS address 0
+  // and a table address is just the perm result (no base to add).
+  __shared__ __attribute__((aligned(16))) unsigned char lut[kLutBytes];
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int S = 2 * G;
+  const int SP = padded_slots(S);
+  const int segs = SP > 64 ? SP >> 6 : 1;   // waves per row
   const int K = G * kGroup;
-  unsigned char* lut = smem;
-  uint16_t* xs = reinterpret_cast<uint16_t*>(smem + kLutBytes);
-  uint32_t* xsw = reinterpret_cast<uint32_t*>(xs);
-  float* gsum = reinterpret_cast<float*>(smem + kLutBytes + 4 * kXStrideDw * G);
-  int* rp = reinterpret_cast<int*>(gsum + G);
-  uint16_t* rowof = reinterpret_cast<uint16_t*>(rp + rows_per_wg + 1);   // record -> row in block
-  const int rowof_cap = rows_per_wg * G;
-  float* part = reinterpret_cast<float*>(
-      (reinterpret_cast<uintptr_t>(rowof + rowof_cap) + 15) & ~static_cast<uintptr_t>(15));
-  const int PS = part_stride(2 * G);
+  uint32_t* xsw = reinterpret_cast<uint32_t*>(smem);
+  // Plane-0 sum of every (row, wave of the row), then two values per record
+  // (its halves).  Pointers derive from the LDS base by plain offsets, so
+  // accesses stay LDS instructions.
+  float* rowsum = reinterpret_cast<float*>(smem + 4 * kXStrideDw * G);
+  float* recval = rowsum + rows_per_wg * segs;
+  const int rec_cap = rows_per_wg * G;   // records a block can hold
 
   const int tid = threadIdx.x;
   const int T = nthreads;   // == blockDim.x, without a load of the dispatch packet
-  const int nw = T >> 6;
 
   // Which matrix this workgroup serves: the first workgroups of matrices
   // 1..7 arrive in SGPRs (unused ones are INT32_MAX), so the matrix record
@@ -263,58 +322,50 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   // The whole record in one batch of scalar loads and one wait (left to
   // itself the compiler fetches fields at their first use, one round trip
   // each).
-  const GemvMat M = mats.m[sel];
+  const GemvMat M = args.m[sel];
+  int hk0 = 0, hk1 = 0;
+  if constexpr (kHostRanges) {
+    hk0 = args.rec_begin[w + sel];
+    hk1 = args.rec_begin[w + sel + 1];
+  }
   asm volatile("" ::"s"(M.codes0), "s"(M.scale0), "s"(M.rowptr1), "s"(M.gidx1), "s"(M.codes1), "s"(M.offset1),
-               "s"(M.scale1), "s"(M.y), "s"(M.n_out), "s"(M.nnz1), "s"(M.wg_begin));
+               "s"(M.scale1), "s"(M.y), "s"(M.n_out), "s"(M.nnz1), "s"(M.wg_begin), "s"(hk0), "s"(hk1));
   __builtin_amdgcn_sched_barrier(0);
   void* const yp = M.y;
   const int row_begin = (w - M.wg_begin) * rows_per_wg;
   const int row_end = min(M.n_out, row_begin + rows_per_wg);
   const int nrb = row_end - row_begin;
 
-  const bool active = tid < ri * S;
-  const int sl = active ? tid % S : 0;   // half-group slot within the row
-  const int g = sl >> 1;
+  const bool in_rows = tid < ri * SP;
+  const int sl = in_rows ? tid % SP : 0;   // half-group slot within the row
+  const bool active = in_rows && sl < S;
+  const int g = active ? sl >> 1 : 0;
   const int h = sl & 1;
-  const int rl = active ? tid / S : 0;
+  const int rl = in_rows ? tid / SP : 0;
   const uint32_t slot = (uint32_t)(tid & (kRep - 1)) << 4;
   const bool has_rec = M.nnz1 > 0;
 
-  // 1. CSR slice and record range (loaded first: waiting for them waits for
-  //    nothing else).  Without records, x stands in as a readable address.
-  const int* rpp = has_rec ? M.rowptr1 + row_begin : reinterpret_cast<const int*>(x);
-  const int rp_mine = rpp[has_rec ? min(tid, nrb) : 0];
-  const int k0 = rpp[0];
-  const int k1 = rpp[has_rec ? nrb : 0];
-  // 2. x.
-  uint4 xv[kXLoads];
-#pragma unroll
-  for (int q = 0; q < kXLoads; ++q) xv[q] = reinterpret_cast<const uint4*>(x)[min(tid + q * T, K / 8 - 1)];
-  // Keep the issue order = the order of need: neither the optimiser nor the
-  // scheduler may move loads across these points (no instruction emitted).
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_sched_barrier(0);
-  // 3. Every plane-0 pass of this lane.
-  const uint32_t ngroups = (uint32_t)M.n_out * (uint32_t)G;
-  const uint8_t* body0 = M.codes0 + kHalfBytes * h;
-  const uint8_t* tail0 = M.codes0 + (size_t)(kMainBytes * ngroups) + h;
-  constexpr int kEarly = kEarlyMax < kPasses ? kEarlyMax : kPasses;
-  Pass buf[kPasses];
-  auto issue_pass = [&](int d) {
-    const int r = min(row_begin + rl + d * ri, row_end - 1);
-    load_pass(buf[d], body0, tail0, M.scale0, (uint32_t)r * (uint32_t)G + (uint32_t)g);
-  };
-#pragma unroll
-  for (int d = 0; d < kEarly; ++d) issue_pass(d);
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_sched_barrier(0);
-  // 4. Record halves (two threads per record), spread across the waves:
-  //    loaded here when few passes leave registers to spare, else after
-  //    plane 0.
-  constexpr bool kPreRec = kPasses <= 2;
-  const int item = (tid & 63) * nw + (tid >> 6);
-  const int hh = item & 1;
-  const int kr = k0 + (item >> 1);
+  // 1. Row pointers of this block: thread t < nrb reads the bounds of row t
+  //    (it sums that row's records at the end); without records x stands in
+  //    as a readable address.
+  const int* rpb = has_rec ? M.rowptr1 + row_begin : reinterpret_cast<const int*>(x);
+  const int tr = has_rec ? min(tid, nrb - 1) : 0;
+  const int rpa = rpb[tr];
+  const int rpz = rpb[has_rec ? tr + 1 : 0];
+  int k0, k1;
+  if constexpr (kHostRanges) {
+    k0 = hk0;
+    k1 = hk1;
+  } else {
+    k0 = rpb[0];
+    k1 = rpb[has_rec ? nrb : 0];
+  }
+  // Record halves: two consecutive threads per record, so that the record
+  // work occupies as few waves as possible (an LDS instruction costs the
+  // same however few of its lanes are active).
+  const int hh = tid & 1;
+  const int kr = k0 + (tid >> 1);
+  const int per_sweep = T >> 1;
   // Without records, plane-0 arrays stand in as readable addresses (the
   // loaded values are ignored).
   RecSrc MR;
@@ -327,10 +378,37 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   RecHalf rec;
   // Threads past the block's records reload its last record (no extra
   // cache lines); the values are ignored.
-  const int k_last = min(max(k1 - 1, k0), kmax);
-  if constexpr (kPreRec) load_rec_half(rec, MR, (uint32_t)max(min(kr, k_last), 0), has_rec ? hh : 0);
+  auto rec_index = [&](int k) -> uint32_t { return (uint32_t)max(min(k, min(max(k1 - 1, k0), kmax)), 0); };
+  // 2. x.
+  uint4 xv[kXLoads];
+#pragma unroll
+  for (int q = 0; q < kXLoads; ++q) xv[q] = reinterpret_cast<const uint4*>(x)[min(tid + q * T, K / 8 - 1)];
+  // Keep the issue order = the order of need: neither the optimiser nor the
+  // scheduler may move loads across these points (no instruction emitted).
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  // 3. With host ranges the first sweep of records needs no row pointer.
+  if constexpr (kHostRanges) load_rec_half(rec, MR, rec_index(kr), has_rec ? hh : 0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  // 4. Every plane-0 pass of this lane.
+  const uint32_t ngroups = (uint32_t)M.n_out * (uint32_t)G;
+  const uint8_t* body0 = M.codes0 + kHalfBytes * h;
+  const uint8_t* tail0 = M.codes0 + (size_t)(kMainBytes * ngroups) + h;
+  Pass buf[kPasses];
+#pragma unroll
+  for (int d = 0; d < kPasses; ++d) {
+    const int r = min(row_begin + rl + d * ri, row_end - 1);
+    load_pass(buf[d], body0, tail0, M.scale0, (uint32_t)r * (uint32_t)G + (uint32_t)g);
+  }
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  // 5. Without host ranges: the first sweep of records once the range is
+  //    known, when few passes leave registers to spare (else after plane 0).
+  constexpr bool kPreRec = kHostRanges || kPasses <= 2;
+  if constexpr (!kHostRanges && kPreRec) load_rec_half(rec, MR, rec_index(kr), has_rec ? hh : 0);
 
-  // Set-up in LDS.
+  // Set-up in LDS: x and the table.
 #pragma unroll
   for (int q = 0; q < kXLoads; ++q) {
     // 8 halves: group i / 16, dwords 4 (i % 16) ..  Unconditional (threads
@@ -343,152 +421,88 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
     d[2] = xv[q].z;
     d[3] = xv[q].w;
   }
-  if (tid < 256) {
-    const uint4 e = lut_entry(tid);
+  // One thread per code writes its 16 copies; at step q thread c writes copy
+  // (q + c) % 16, so the 16 lanes of an LDS pass hit 16 different bank
+  // quads.
+  for (int c = tid; c < 256; c += T) {
+    const uint4 e = lut_entry(c);
 #pragma unroll
-    for (int q = 0; q < kRep; ++q) reinterpret_cast<uint4*>(lut)[tid * kRep + q] = e;
+    for (int q = 0; q < kRep; ++q) reinterpret_cast<uint4*>(lut)[c * kRep + ((q + c) & (kRep - 1))] = e;
   }
-  if (has_rec && tid <= nrb) rp[tid] = rp_mine;
   __syncthreads();
-  if constexpr (kEarly < kPasses) {
-    asm volatile("" ::: "memory");
-#pragma unroll
-    for (int d = kEarly; d < kPasses; ++d) issue_pass(d);
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_sched_barrier(0);
-  }
 
-  // Row of every record of the block (replaces a search per record).
-  if (has_rec && tid < nrb) {
-    const int kb = max(rp[tid], k0), ke = min(rp[tid + 1], k1);
-    for (int k = kb; k < ke && k - k0 < rowof_cap; ++k) rowof[k - k0] = (uint16_t)tid;
-  }
-
-  // This lane's activations: 12 body bytes (inputs 60h + 5j ..) and the tail
-  // byte (inputs 120 + 5h ..), three fp16 pairs per byte.
+  // This lane's activations.
   uint32_t xr[kLaneBytes][3];
-  {
-    const uint32_t* xd = xsw + kXStrideDw * g + 30 * h;   // inputs 60 h ..
-#pragma unroll
-    for (int j = 0; j < kHalfBytes; j += 2) {   // bytes j, j+1: inputs 5j .. 5j+9 = dwords 5j/2 ..
-      const int q = 5 * j / 2;
-      const uint32_t d0 = xd[q], d1 = xd[q + 1], d2 = xd[q + 2], d3 = xd[q + 3], d4 = xd[q + 4];
-      xr[j][0] = d0;
-      xr[j][1] = d1;
-      xr[j][2] = d2 & 0xFFFFu;
-      xr[j + 1][0] = __builtin_amdgcn_alignbit(d3, d2, 16);
-      xr[j + 1][1] = __builtin_amdgcn_alignbit(d4, d3, 16);
-      xr[j + 1][2] = d4 >> 16;
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    const uint16_t* xt = xs + 2 * kXStrideDw * g + 120 + 5 * h;
-    uint32_t e[5];
-#pragma unroll
-    for (int i = 0; i < 5; ++i) e[i] = (120 + 5 * h + i < kGroup) ? (uint32_t)xt[i] : 0u;
-    xr[kHalfBytes][0] = e[0] | (e[1] << 16);
-    xr[kHalfBytes][1] = e[2] | (e[3] << 16);
-    xr[kHalfBytes][2] = e[4];
-  }
-  // Group sums for the offsets: each lane sums its half, the pair combines
-  // (half 0 first on both lanes, so both get the same bits).
-  {
-    float s0 = 0.f, s1 = 0.f, s2 = 0.f;
-#pragma unroll
-    for (int j = 0; j < kLaneBytes; ++j) {
-      s0 = fdot2(xr[j][0], 0x3C003C00u, s0);
-      s1 = fdot2(xr[j][1], 0x3C003C00u, s1);
-      s2 = fdot2(xr[j][2], 0x3C003C00u, s2);
-    }
-    const float s = (s0 + s1) + s2;
-    const float other = __builtin_bit_cast(   // lane ^ 1 (quad_perm 1,0,3,2)
-        float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, s), 0xB1, 0xF, 0xF, false));
-    const float tot = h == 0 ? s + other : other + s;
-    if (active && rl == 0 && h == 0) gsum[g] = tot;
-  }
+  load_xr(xr, xsw, g, h);
 
-  // Plane 0: part[row][slot] = s0 * sum_i t0 x over the half-group.
+  // Plane 0, one row per pass: s0 * sum_i t0 x over each half-group, summed
+  // over the row's lanes of this wave.
+  const int seg = SP < 64 ? SP : 64;
 #pragma unroll
   for (int d = 0; d < kPasses; ++d) {
-    const float p = code_dot<kLaneBytes>(lut, slot, buf[d].w, [&](int j, int q) { return xr[j][q]; });
-    if (active && rl + d * ri < nrb) part[(rl + d * ri) * PS + sl] = p * h2f(buf[d].sc);
+    const int row = rl + d * ri;
+    float v = code_dot(lut, slot, buf[d].w, xr) * h2f(buf[d].sc);
+    // Pin the value here: otherwise the dot products sink into the guarded
+    // store below while their table reads cannot, and the reads' results of
+    // every pass stay live at once.
+    asm volatile("" : "+v"(v));
+    v = (active && row < nrb) ? v : 0.f;
+    const float sum = segment_sum(v, seg);
+    if (in_rows && row < nrb && (sl & (seg - 1)) == 0) rowsum[row * segs + (sl >> 6)] = sum;
     __builtin_amdgcn_sched_barrier(0);   // keep passes apart: bounds the LUT reads in flight
   }
-  // Plane-0 passes beyond kPasses (only when the host could not fit a
-  // matrix into one round of workgroups with kPasses passes).
-  for (int d = kPasses; active && rl + d * ri < nrb; ++d) {
-    Pass q;
-    load_pass(q, body0, tail0, M.scale0, (uint32_t)(row_begin + rl + d * ri) * (uint32_t)G + (uint32_t)g);
-    const float p = code_dot<kLaneBytes>(lut, slot, q.w, [&](int j, int qq) { return xr[j][qq]; });
-    part[(rl + d * ri) * PS + sl] = p * h2f(q.sc);
-  }
 
-  // Plane 1: each record half adds to its (row, half-group) slot.
+  // Plane 1: each record half stores its value (records of a block are
+  // contiguous, so a record's slot is its index in the block).
   if (has_rec) {
-    __syncthreads();   // plane-0 partials and group sums are in LDS
-    const int per_sweep = T >> 1;
     for (int k = kr, first = 1; k < k1; k += per_sweep, first = 0) {
-      if (!kPreRec || !first) load_rec_half(rec, MR, (uint32_t)min(max(k, 0), kmax), hh);
-      if (k < 0 || k - k0 >= rowof_cap) continue;
-      const int lo = min((int)rowof[k - k0], nrb - 1);
-      const float v = record_half_value(lut, slot, xs, gsum, rec, hh, G);
-      float* dst = part + lo * PS + 2 * min((int)rec.g, G - 1) + hh;
-      *dst = *dst + v;
+      if (!kPreRec || !first) load_rec_half(rec, MR, rec_index(k), hh);
+      if (k >= 0 && k - k0 < rec_cap) recval[2 * (k - k0) + hh] = record_half_value(lut, slot, xsw, rec, hh, G);
     }
   }
   __syncthreads();
 
-  // Row sums: one thread per row, four independent accumulators over the
-  // row's partials in a fixed order.
-  for (int rr = tid; rr < nrb; rr += T) {
-    const float4* pr = reinterpret_cast<const float4*>(part + rr * PS);
-    float4 a = {0.f, 0.f, 0.f, 0.f};
-    const int n4 = S >> 2;
-    for (int c = 0; c < n4; ++c) {
-      const float4 v = pr[c];
-      a.x += v.x;
-      a.y += v.y;
-      a.z += v.z;
-      a.w += v.w;
+  // Row totals, one thread per row in a fixed order: the row's wave sums,
+  // then its records (half 0 + half 1) in index order.
+  if (tid < nrb) {
+    float a = rowsum[tid * segs];
+    for (int c = 1; c < segs; ++c) a += rowsum[tid * segs + c];
+    if (has_rec) {
+      const int kb = max(rpa, k0), ke = min(min(rpz, k1), k0 + rec_cap);
+      for (int k = kb; k < ke; ++k) a += recval[2 * (k - k0)] + recval[2 * (k - k0) + 1];
     }
-    if (S & 2) {   // S = 2G is even: at most two trailing partials
-      a.x += part[rr * PS + 4 * n4];
-      a.y += part[rr * PS + 4 * n4 + 1];
-    }
-    const float sum = (a.x + a.y) + (a.z + a.w);
-    if (out_f32)
-      reinterpret_cast<float*>(yp)[row_begin + rr] = sum;
-    else
-      reinterpret_cast<uint16_t*>(yp)[row_begin + rr] = __builtin_bit_cast(uint16_t, (_Float16)sum);
+    store_y(yp, row_begin + tid, a, out_f32);
   }
 }
 
 typedef void (*GemvKernel)(const uint16_t*, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t,
-                           int32_t, int32_t, int32_t, int32_t, const GemvMats);
+                           int32_t, int32_t, int32_t, int32_t, const GemvArgs);
 
 constexpr int kPassChoices[] = {1, 2, 3, 4, 6, 8};
 constexpr int kNumPass = 6;
 constexpr int kXChoices[] = {1, 2, 4};
 
-template <int PI, int XI>
+template <int PI, int XI, bool HR>
 constexpr GemvKernel kernel_at() {
-  return gemv_kernel<kPassChoices[PI], kXChoices[XI]>;
+  return gemv_kernel<kPassChoices[PI], kXChoices[XI], HR>;
 }
 
-GemvKernel select_kernel(int pi, int xi) {
+template <bool HR>
+GemvKernel select_kernel_hr(int pi, int xi) {
   static const GemvKernel table[kNumPass][3] = {
-      {kernel_at<0, 0>(), kernel_at<0, 1>(), kernel_at<0, 2>()},
-      {kernel_at<1, 0>(), kernel_at<1, 1>(), kernel_at<1, 2>()},
-      {kernel_at<2, 0>(), kernel_at<2, 1>(), kernel_at<2, 2>()},
-      {kernel_at<3, 0>(), kernel_at<3, 1>(), kernel_at<3, 2>()},
-      {kernel_at<4, 0>(), kernel_at<4, 1>(), kernel_at<4, 2>()},
-      {kernel_at<5, 0>(), kernel_at<5, 1>(), kernel_at<5, 2>()},
+      {kernel_at<0, 0, HR>(), kernel_at<0, 1, HR>(), kernel_at<0, 2, HR>()},
+      {kernel_at<1, 0, HR>(), kernel_at<1, 1, HR>(), kernel_at<1, 2, HR>()},
+      {kernel_at<2, 0, HR>(), kernel_at<2, 1, HR>(), kernel_at<2, 2, HR>()},
+      {kernel_at<3, 0, HR>(), kernel_at<3, 1, HR>(), kernel_at<3, 2, HR>()},
+      {kernel_at<4, 0, HR>(), kernel_at<4, 1, HR>(), kernel_at<4, 2, HR>()},
+      {kernel_at<5, 0, HR>(), kernel_at<5, 1, HR>(), kernel_at<5, 2, HR>()},
   };
   return table[pi][xi];
 }
 
 struct DeviceInfo {
   int cus = 0;
-  bool attr_set[kNumPass][3] = {};
+  bool attr_set[2][kNumPass][3] = {};
 };
 
 DeviceInfo& device_info() {
@@ -498,10 +512,12 @@ DeviceInfo& device_info() {
   return info[dev & 63];
 }
 
-size_t lds_bytes(int G, int rb_max) {
-  const size_t head = (size_t)kLutBytes + 4 * (size_t)kXStrideDw * G + 4 * (size_t)G + 4 * (size_t)(rb_max + 1) +
-                      2 * (size_t)rb_max * G;
-  return ((head + 15) & ~(size_t)15) + 4 * (size_t)rb_max * part_stride(2 * G);
+// LDS bytes of one workgroup: table, x, wave sums of every row, two values
+// per record.
+size_t lds_bytes(int G, int rows) {
+  const int SP = padded_slots(2 * G);
+  const int segs = SP > 64 ? SP / 64 : 1;
+  return (size_t)kLutBytes + 4 * (size_t)kXStrideDw * G + 4 * (size_t)rows * segs + 8 * (size_t)rows * G;
 }
 
 }  // namespace
@@ -519,62 +535,45 @@ hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n, const uint16_t*
 
   const int G = ms[0].n_groups;
   const int S = 2 * G;
-  int64_t total_rows = 0;
-  for (int i = 0; i < n; ++i) total_rows += ms[i].n_out;
-
-  // LDS: table + x + group sums + CSR slice + partials.  Two workgroups per
-  // CU when they fit in half of the 160 KiB (then at most 512 threads each,
-  // 16 waves per CU in all); otherwise one of up to 1024 threads.
-  const size_t fixed = lds_bytes(G, 0) + 16;   // + alignment of the partials
-  const size_t per_row = 4 * (size_t)part_stride(S) + 2 * (size_t)G + 4;
-  const size_t half_lds = 80 * 1024, full_lds = 160 * 1024;
-  const int ri512 = 512 / S;
-  const int wgs_per_cu = (ri512 >= 1 && fixed + per_row * ri512 <= half_lds) ? 2 : 1;
-  const size_t budget = wgs_per_cu == 2 ? half_lds : full_lds;
-  const int t_max = wgs_per_cu == 2 ? 512 : kMaxThreads;
-
-  // Threads per workgroup: the multiple of 64 in [256, t_max] leaving the
-  // fewest lanes without a half-group; the larger wins ties.
-  int T = 0;
-  double best = -1.0;
-  for (int t = 256; t <= t_max; t += 64) {
-    const double used = (double)((t / S) * S) / t;
-    if (used >= best - 1e-9) {
-      best = used;
-      T = t;
+  const int SP = padded_slots(S);
+  // Launch shape: one workgroup per CU (the 64 KiB table leaves no room for
+  // two), T threads (a multiple of SP and of 64, at least 256) and passes
+  // per lane.  Chosen from measurements on MI355X: first one round of
+  // workgroups, then the fewest rows per workgroup (the most CUs busy), then
+  // the least of waves + 4 * passes (a wave's serial pass chain costs about
+  // four times its share of the set-up).
+  int T = 0, pi = -1;
+  int64_t best_rounds = 0;
+  int best_rows = 0, best_score = 0;
+  for (int t = 256; t <= kMaxThreads; t += 64) {
+    if (t % SP != 0 || (G * kGroup / 8 + t - 1) / t > kXChoices[2]) continue;
+    const int r = t / SP;
+    for (int p = 0; p < kNumPass; ++p) {
+      const int rows = kPassChoices[p] * r;
+      if (lds_bytes(G, rows) > 160 * 1024 || rows > t) break;   // one thread per row at the end
+      int64_t nwg = 0;
+      for (int i = 0; i < n; ++i) nwg += (ms[i].n_out + rows - 1) / rows;
+      const int64_t rounds = (nwg + di.cus - 1) / di.cus;
+      const int score = t / 64 + 4 * kPassChoices[p];
+      if (pi < 0 || rounds < best_rounds ||
+          (rounds == best_rounds && (rows < best_rows || (rows == best_rows && score < best_score)))) {
+        T = t;
+        pi = p;
+        best_rounds = rounds;
+        best_rows = rows;
+        best_score = score;
+      }
     }
   }
-  const int ri = T / S;
-
-  // Passes per lane: enough for one round of workgroups, capped by the
-  // compiled choices, by LDS for the partials and by one CSR entry per thread.
-  int max_rows = (int)((budget - fixed) / per_row);
-  if (max_rows > T - 1) max_rows = T - 1;
-  const int max_pass = max_rows / ri < 1 ? 1 : max_rows / ri;
-  const int64_t target_wgs = (int64_t)di.cus * wgs_per_cu;
-  int want = (int)((total_rows + target_wgs * ri - 1) / (target_wgs * ri));
-  if (want > max_pass) want = max_pass;
-  int pi = 0;
-  while (pi < kNumPass - 1 && kPassChoices[pi] < want) ++pi;
-  int passes = kPassChoices[pi];
-  if (passes > max_pass) {   // largest compiled choice that fits
-    while (pi > 0 && kPassChoices[pi] > max_pass) --pi;
-    passes = kPassChoices[pi];
-  }
+  if (pi < 0) return hipErrorInvalidValue;
+  const int ri = T / SP;
+  const int passes = kPassChoices[pi];
   const int rows_per_wg = passes * ri;
   const int xloads = (G * kGroup / 8 + T - 1) / T;
   const int xi = xloads <= 1 ? 0 : (xloads <= 2 ? 1 : 2);
   if (kXChoices[xi] < xloads) return hipErrorInvalidValue;
 
-  const GemvKernel kern = select_kernel(pi, xi);
-  if (!di.attr_set[pi][xi]) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (e != hipSuccess) return e;
-    di.attr_set[pi][xi] = true;
-  }
-
-  GemvMats A = {};
+  GemvArgs A = {};
   int32_t wb[TQ_MAX_GROUPED];
   int wg = 0;
   for (int i = 0; i < TQ_MAX_GROUPED; ++i) {
@@ -595,7 +594,38 @@ hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n, const uint16_t*
     wb[i] = wg;
     wg += (ms[i].n_out + rows_per_wg - 1) / rows_per_wg;
   }
-  hipLaunchKernelGGL(kern, dim3(wg), dim3(T), lds_bytes(G, rows_per_wg), s, x, G, ri, rows_per_wg,
+
+  // Record ranges from the host copies of the row pointers, when every
+  // matrix with records has one and the table fits.
+  bool host_ranges = wg + n <= kMaxRangeEntries;
+  for (int i = 0; i < n && host_ranges; ++i)
+    if (ms[i].nnz1 > 0 && ms[i].rowptr1_host == nullptr) host_ranges = false;
+  if (host_ranges) {
+    for (int i = 0; i < n; ++i) {
+      const int nwg = (ms[i].n_out + rows_per_wg - 1) / rows_per_wg;
+      int32_t* t = A.rec_begin + A.m[i].wg_begin + i;
+      const int64_t nnz = ms[i].nnz1;
+      for (int j = 0; j <= nwg; ++j) {
+        int64_t v = 0;
+        if (nnz > 0) {
+          const int64_t r = (int64_t)j * rows_per_wg < ms[i].n_out ? (int64_t)j * rows_per_wg : ms[i].n_out;
+          v = ms[i].rowptr1_host[r];
+          v = v < 0 ? 0 : (v > nnz ? nnz : v);   // in bounds whatever the host copy holds
+        }
+        t[j] = (int32_t)v;
+      }
+    }
+  }
+
+  const int hr = host_ranges ? 1 : 0;
+  const GemvKernel kern = host_ranges ? select_kernel_hr<true>(pi, xi) : select_kernel_hr<false>(pi, xi);
+  if (!di.attr_set[hr][pi][xi]) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - kLutBytes);
+    if (e != hipSuccess) return e;
+    di.attr_set[hr][pi][xi] = true;
+  }
+  hipLaunchKernelGGL(kern, dim3(wg), dim3(T), lds_bytes(G, rows_per_wg) - kLutBytes, s, x, G, ri, rows_per_wg,
                      out_f32 ? 1 : 0, wb[1], wb[2], wb[3], wb[4], wb[5], wb[6], wb[7], T, A);
   return hipGetLastError();
 }

@@ -56,6 +56,7 @@ tq_status check_matrix(const tq_matrix* m, MatDev* d) {
   d->codes1 = m->nnz1 > 0 ? m->codes1 : nullptr;
   d->offset1 = m->nnz1 > 0 ? m->offset1 : nullptr;
   d->scale1 = m->nnz1 > 0 ? m->scale1 : nullptr;
+  d->rowptr1_host = m->nnz1 > 0 ? m->rowptr1_host : nullptr;
   d->n_out = (int32_t)m->n_out;
   d->n_groups = (int32_t)G;
   return TQ_OK;

@@ -1,4 +1,4 @@
-// Internal interface between the host entry points (tq_api.cpp) and the
+// Internal interface between the host entry points (tq_api.hip) and the
 // kernel launchers (codec.hip, gemv.hip, gemm.hip).  Every launcher assumes
 // its arguments were already checked on the host and returns the status of
 // the launch.
@@ -25,6 +25,7 @@ struct MatDev {
   const uint8_t* codes1;
   const uint16_t* offset1;
   const uint16_t* scale1;
+  const int32_t* rowptr1_host;   // host memory, may be NULL
   int64_t nnz1;
   int32_t n_out;
   int32_t n_groups;   // groups per row, K / 128

@@ -47,6 +47,7 @@ class TqMatrix(ctypes.Structure):
         ("codes1", ctypes.c_void_p),
         ("offset1", ctypes.c_void_p),
         ("scale1", ctypes.c_void_p),
+        ("rowptr1_host", ctypes.c_void_p),
     ]
 
 
@@ -116,6 +117,7 @@ class PackedLinear:
     codes1: torch.Tensor = None   # uint8 [26 * nnz1]
     offset1: torch.Tensor = None  # float16 [nnz1]
     scale1: torch.Tensor = None   # float16 [nnz1]
+    rowptr1_host: torch.Tensor = None  # optional host copy of rowptr1 (int32, CPU)
 
     @property
     def nnz1(self):
@@ -137,6 +139,8 @@ class PackedLinear:
             m.codes1 = self.codes1.data_ptr()
             m.offset1 = self.offset1.data_ptr()
             m.scale1 = self.scale1.data_ptr()
+            if self.rowptr1_host is not None:
+                m.rowptr1_host = self.rowptr1_host.data_ptr()
         return m
 
     def nbytes(self):
@@ -148,8 +152,10 @@ class PackedLinear:
         return b
 
     @classmethod
-    def from_inputs(cls, inp, device="cuda", stream=None):
-        """Upload unpacked inputs (trits, scales, CSR) and pack them on the GPU."""
+    def from_inputs(cls, inp, device="cuda", stream=None, host_rowptr=True):
+        """Upload unpacked inputs (trits, scales, CSR) and pack them on the GPU.
+        With host_rowptr the row pointers are also kept in host memory (see
+        tq_matrix.rowptr1_host)."""
         dev = torch.device(device)
         t0 = torch.from_numpy(inp.t0.reshape(-1, GROUP)).to(dev)
         codes0 = tq_pack(t0, stream=stream)
@@ -164,6 +170,8 @@ class PackedLinear:
                 offset1=torch.from_numpy(inp.mu1).to(dev),
                 scale1=torch.from_numpy(inp.s1).to(dev),
             )
+            if host_rowptr:
+                kw["rowptr1_host"] = torch.from_numpy(inp.rowptr1.astype("int32")).contiguous()
         return cls(inp.n_out, inp.n_in, codes0, torch.from_numpy(inp.s0).to(dev), **kw)
 
 

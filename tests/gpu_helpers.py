@@ -18,7 +18,7 @@ def log(msg):
 class Case:
     """One packed linear on both sides, built from the same unpacked inputs."""
 
-    def __init__(self, inp, device="cuda"):
+    def __init__(self, inp, device="cuda", host_rowptr=True):
         self.inp = inp
         self.c0, b0 = codec.pack(inp.t0.reshape(-1, 128))
         if inp.nnz1:
@@ -26,7 +26,7 @@ class Case:
         else:
             self.c1, b1 = np.zeros(0, np.uint8), 0
         assert b0 == 0 and b1 == 0
-        self.gpu = tq.PackedLinear.from_inputs(inp, device)
+        self.gpu = tq.PackedLinear.from_inputs(inp, device, host_rowptr=host_rowptr)
 
     def oracle_args(self):
         i = self.inp

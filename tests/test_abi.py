@@ -9,6 +9,7 @@ wrongly accepted call could never reach a device.
 import ctypes
 import os
 import re
+import subprocess
 
 import pytest
 import torch
@@ -42,16 +43,27 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert tq.tq_abi_version() == 1
+    assert tq.tq_abi_version() == 2
     for s in range(6):
         assert tq.tq_status_string(s).startswith(tq.STATUS[s])
     assert "unknown" in tq.tq_status_string(42)
 
 
-def test_matrix_struct_layout_matches_header():
-    # 2 x int64, 2 x int32, 2 pointers, int64, 5 pointers
-    assert ctypes.sizeof(tq.TqMatrix) == 8 * 2 + 4 * 2 + 8 * 2 + 8 + 8 * 5
-    assert tq.TqMatrix.nnz1.offset == 40
+def test_matrix_struct_layout_matches_header(tmp_path):
+    """The ctypes mirror of tq_matrix has the C compiler's layout."""
+    fields = [f[0] for f in tq.TqMatrix._fields_]
+    src = tmp_path / "layout.c"
+    src.write_text('#include <stddef.h>\n#include <stdio.h>\n#include "tq.h"\nint main(void) {\n'
+                   '  printf("size %zu\\n", sizeof(tq_matrix));\n'
+                   + "".join(f'  printf("{f} %zu\\n", offsetof(tq_matrix, {f}));\n' for f in fields)
+                   + "  return 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = dict(line.split() for line in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                       check=True).stdout.splitlines())
+    assert int(out["size"]) == ctypes.sizeof(tq.TqMatrix)
+    for f in fields:
+        assert int(out[f]) == getattr(tq.TqMatrix, f).offset, f
 
 
 FAKE = 0x7F0000000000   # 256-byte aligned, never dereferenced

@@ -107,6 +107,26 @@ def test_grouped_matches_single_bitwise():
         assert_within_bound(yg.cpu().numpy(), want, c.bound(x), "grouped")
 
 
+@pytest.mark.parametrize("n_out,n_in,f2", [
+    (4096, 4096, 0.1), (12288, 4096, 0.1), (4096, 12288, 0.1), (1024, 4096, 0.1),
+    (3000, 640, 0.1), (100, 32768, 0.05), (65, 384, 0.5), (1, 128, 1.0),
+])
+def test_device_row_pointers_match_host_ranges(n_out, n_in, f2):
+    """Without the host copy of the row pointers the kernel reads the record
+    ranges itself and handles records after plane 0; the bits are the same."""
+    inp = synth.linear(n_out, n_in, f2, (11, n_out, n_in, 0))
+    x = synth.activations(n_in, (11, n_out, n_in, 1), outlier_frac=0.01)
+    with_host = Case(inp)
+    device_only = Case(inp, host_rowptr=False)
+    assert device_only.gpu.rowptr1_host is None
+    got = run_gemv(device_only, x, out_f32=True)
+    ref = run_gemv(with_host, x, out_f32=True)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+    want = with_host.oracle_gemm(x[None])[0]
+    r = assert_within_bound(got, want, with_host.bound(x), f"device ranges {n_out}x{n_in}")
+    log(f"device ranges {n_out}x{n_in} f2={f2}: max err/bound {r:.3g}")
+
+
 @pytest.mark.parametrize("layer", [0, 35])
 def test_decode_step_layers_sampled(layer):
     """Layers of the 36-layer stack, in the grouped stages the benchmark runs."""
