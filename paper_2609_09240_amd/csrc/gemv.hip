@@ -11,12 +11,14 @@
 //   tail byte 24+h (inputs 120+5h ..).  Rows are laid on SP lanes, SP = S
 //   rounded up to a divisor or a multiple of 64, so that no row straddles a
 //   wave boundary; a workgroup of T threads covers RI = T / SP rows per pass
-//   and thread t always owns half-group t % SP, so its activations stay in 39
-//   VGPRs for the whole launch, laid out per code byte j as the fp16 pairs
-//   (x5j, x5j+1), (x5j+2, x5j+3), (x5j+4, 0).
-// * Decode.  A 256-entry table maps a code to the same three pairs of fp16
-//   patterns (+1 = 0x3C00, -1 = 0xBC00, 0 = 0); three v_dot2_f32_f16 then
-//   accumulate the sign-selected activations in fp32.  The table is
+//   and thread t always owns half-group t % SP, so its activations stay in 33
+//   VGPRs for the whole launch: per pair of code bytes (j, j+1) the fp16
+//   pairs (x0, x1), (x2, x3) of each byte and (x4 of j, x4 of j+1); for the
+//   tail byte (x0, x1), (x2, x3), (x4, 0).
+// * Decode.  A 256-entry table maps a code to four dwords of fp16 patterns
+//   (+1 = 0x3C00, -1 = 0xBC00, 0 = 0): (t0, t1), (t2, t3), (t4, 0), (0, t4).
+//   A pair of bytes takes two 16-byte table reads and five v_dot2_f32_f16
+//   (the fifth on (t4 of j) | (t4 of j+1)), accumulating in fp32.  The table is
 //   replicated kRep = 16 times in LDS (copy q of code c at byte 16 (16 c + q),
 //   64 KiB); a lane reads copy lane % 16 (12 bytes), so lanes read together
 //   sit on different banks whatever codes they hold (four copies cost two to
@@ -79,8 +81,8 @@ __host__ __device__ inline int padded_slots(int S) {
 // ---------------------------------------------------------------- table
 __device__ inline uint32_t trit_pattern(int t) { return t > 0 ? 0x3C00u : (t < 0 ? 0xBC00u : 0u); }
 
-// Table entry of code c: fp16 patterns of (t0, t1), (t2, t3), (t4, 0);
-// codes 243..255 map to zeros.  Computed in registers (no memory access).
+// Table entry of code c: fp16 patterns of (t0, t1), (t2, t3), (t4, 0),
+// (0, t4); codes 243..255 map to zeros.  Computed in registers.
 __device__ inline uint4 lut_entry(int c) {
   uint32_t t[5];
   uint32_t d = (uint32_t)c;
@@ -90,7 +92,7 @@ __device__ inline uint4 lut_entry(int c) {
     t[i] = c < 243 ? trit_pattern((int)(d - 3u * q) - 1) : 0u;
     d = q;
   }
-  return uint4{t[0] | (t[1] << 16), t[2] | (t[3] << 16), t[4], 0u};
+  return uint4{t[0] | (t[1] << 16), t[2] | (t[3] << 16), t[4], t[4] << 16};
 }
 
 // ---------------------------------------------------------------- params
@@ -137,53 +139,68 @@ __device__ inline uint32_t lut_addr(uint32_t w, uint32_t slot) {
   return __builtin_amdgcn_perm(slot, w, 0x0C0C0004u | (B << 8));
 }
 
+// Activation registers of a half-group: 6 pairs of code bytes x 5 dwords,
+// then 3 for the tail byte.
+constexpr int kXrRegs = 33;
+
+// LDS byte address of this lane's table copy for code byte j of w.
+__device__ __attribute__((always_inline)) inline uint32_t code_addr(const uint32_t (&w)[4], int j, uint32_t slot) {
+  switch (j & 3) {
+    case 0: return lut_addr<0>(w[j >> 2], slot);
+    case 1: return lut_addr<1>(w[j >> 2], slot);
+    case 2: return lut_addr<2>(w[j >> 2], slot);
+    default: return lut_addr<3>(w[j >> 2], slot);
+  }
+}
+
 // Dot product of the 13 code bytes of a half-group (byte j in byte j % 4 of
-// w[j / 4]) with activation pairs xr[j][q].
+// w[j / 4]) with its activation registers.
 __device__ __attribute__((always_inline)) inline float code_dot(const unsigned char* lut, uint32_t slot,
                                                                 const uint32_t (&w)[4],
-                                                                const uint32_t (&xr)[kLaneBytes][3]) {
+                                                                const uint32_t (&xr)[kXrRegs]) {
+  typedef uint32_t u4v __attribute__((ext_vector_type(4)));
   float a0 = 0.f, a1 = 0.f, a2 = 0.f;
 #pragma unroll
-  for (int j = 0; j < kLaneBytes; ++j) {
-    uint32_t addr;
-    switch (j & 3) {
-      case 0: addr = lut_addr<0>(w[j >> 2], slot); break;
-      case 1: addr = lut_addr<1>(w[j >> 2], slot); break;
-      case 2: addr = lut_addr<2>(w[j >> 2], slot); break;
-      default: addr = lut_addr<3>(w[j >> 2], slot); break;
-    }
-    const U3 p = *reinterpret_cast<const U3*>(lut + addr);
-    a0 = fdot2(p.x, xr[j][0], a0);
-    a1 = fdot2(p.y, xr[j][1], a1);
-    a2 = fdot2(p.z, xr[j][2], a2);
+  for (int m = 0; m < kHalfBytes / 2; ++m) {
+    // Full 16-byte reads: the 16 lanes served together cover the 64 banks
+    // exactly once, and the fourth dword carries t4 in the high half.
+    const u4v e0 = *reinterpret_cast<const u4v*>(lut + code_addr(w, 2 * m, slot));
+    const u4v e1 = *reinterpret_cast<const u4v*>(lut + code_addr(w, 2 * m + 1, slot));
+    a0 = fdot2(e0.x, xr[5 * m], a0);
+    a1 = fdot2(e0.y, xr[5 * m + 1], a1);
+    a0 = fdot2(e1.x, xr[5 * m + 2], a0);
+    a1 = fdot2(e1.y, xr[5 * m + 3], a1);
+    a2 = fdot2(e0.z | e1.w, xr[5 * m + 4], a2);
   }
+  const U3 e = *reinterpret_cast<const U3*>(lut + code_addr(w, kHalfBytes, slot));
+  a0 = fdot2(e.x, xr[30], a0);
+  a1 = fdot2(e.y, xr[31], a1);
+  a2 = fdot2(e.z, xr[32], a2);
   return (a0 + a1) + a2;
 }
 
 // Activations of half h of group g from the LDS copy of x: 12 body bytes
-// (inputs 60h + 5j ..) and the tail byte (inputs 120 + 5h ..), three fp16
-// pairs per byte; inputs past the group (pad digits) are zero.
-__device__ __attribute__((always_inline)) inline void load_xr(uint32_t (&xr)[kLaneBytes][3], const uint32_t* xsw,
-                                                              int g, int h) {
+// (inputs 60h + 5j ..) and the tail byte (inputs 120 + 5h ..); inputs past
+// the group (pad digits) are zero.
+__device__ __attribute__((always_inline)) inline void load_xr(uint32_t (&xr)[kXrRegs], const uint32_t* xsw, int g,
+                                                              int h) {
   const uint32_t* xd = xsw + kXStrideDw * g + 30 * h;   // inputs 60 h ..
 #pragma unroll
-  for (int j = 0; j < kHalfBytes; j += 2) {   // bytes j, j+1: inputs 5j .. 5j+9 = dwords 5j/2 ..
-    const int q = 5 * j / 2;
-    const uint32_t d0 = xd[q], d1 = xd[q + 1], d2 = xd[q + 2], d3 = xd[q + 3], d4 = xd[q + 4];
-    xr[j][0] = d0;
-    xr[j][1] = d1;
-    xr[j][2] = d2 & 0xFFFFu;
-    xr[j + 1][0] = __builtin_amdgcn_alignbit(d3, d2, 16);
-    xr[j + 1][1] = __builtin_amdgcn_alignbit(d4, d3, 16);
-    xr[j + 1][2] = d4 >> 16;
+  for (int m = 0; m < kHalfBytes / 2; ++m) {   // bytes 2m, 2m+1: inputs 10m .. 10m+9 = dwords 5m ..
+    const uint32_t d0 = xd[5 * m], d1 = xd[5 * m + 1], d2 = xd[5 * m + 2], d3 = xd[5 * m + 3], d4 = xd[5 * m + 4];
+    xr[5 * m] = d0;
+    xr[5 * m + 1] = d1;
+    xr[5 * m + 2] = __builtin_amdgcn_alignbit(d3, d2, 16);
+    xr[5 * m + 3] = __builtin_amdgcn_alignbit(d4, d3, 16);
+    xr[5 * m + 4] = __builtin_amdgcn_perm(d4, d2, 0x07060100u);   // (low half of d2, high half of d4)
   }
   const uint16_t* xt = reinterpret_cast<const uint16_t*>(xsw + kXStrideDw * g) + 120 + 5 * h;
   uint32_t e[5];
 #pragma unroll
   for (int i = 0; i < 5; ++i) e[i] = (120 + 5 * h + i < kGroup) ? (uint32_t)xt[i] : 0u;
-  xr[kHalfBytes][0] = e[0] | (e[1] << 16);
-  xr[kHalfBytes][1] = e[2] | (e[3] << 16);
-  xr[kHalfBytes][2] = e[4];
+  xr[30] = e[0] | (e[1] << 16);
+  xr[31] = e[2] | (e[3] << 16);
+  xr[32] = e[4];
 }
 
 // One pass of plane 0 for one lane: 12 body bytes, 1 tail byte, 1 scale.
@@ -236,46 +253,45 @@ __device__ inline void load_rec_half(RecHalf& r, const RecSrc& M, uint32_t k, in
 __device__ __attribute__((always_inline)) inline float record_half_value(const unsigned char* lut, uint32_t slot,
                                                                          const uint32_t* xsw, const RecHalf& r,
                                                                          int hh, int G) {
-  uint32_t xr[kLaneBytes][3];
+  uint32_t xr[kXrRegs];
   load_xr(xr, xsw, min((int)r.g, G - 1), hh);
   float s0 = 0.f, s1 = 0.f, s2 = 0.f;
 #pragma unroll
-  for (int j = 0; j < kLaneBytes; ++j) {
-    s0 = fdot2(xr[j][0], 0x3C003C00u, s0);
-    s1 = fdot2(xr[j][1], 0x3C003C00u, s1);
-    s2 = fdot2(xr[j][2], 0x3C003C00u, s2);
+  for (int i = 0; i < kXrRegs; i += 3) {
+    s0 = fdot2(xr[i], 0x3C003C00u, s0);
+    s1 = fdot2(xr[i + 1], 0x3C003C00u, s1);
+    s2 = fdot2(xr[i + 2], 0x3C003C00u, s2);
   }
   const float xsum = (s0 + s1) + s2;
   const float p1 = code_dot(lut, slot, r.w, xr);
   return h2f(r.s1) * p1 + h2f(r.mu) * xsum;
 }
 
-// Sum of v over aligned segments of seg lanes (seg a power of two <= 64);
-// every lane of a segment returns the same bits.
+// Sum of v over aligned segments of seg lanes (seg a power of two <= 64),
+// exact in the last lane of each segment (and in every lane for seg <= 16).
+// Butterflies inside 16-lane rows, then row broadcasts: a fixed order, so
+// the result is bit-reproducible.
 __device__ __attribute__((always_inline)) inline float segment_sum(float v, int seg) {
-  auto dpp = [](float a, int ctrl) -> float {
+  auto shuffled = [](float a, int ctrl, int row_mask) -> float {
+    const int x = __builtin_bit_cast(int, a);
     int r;
     switch (ctrl) {
-      case 0: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, a), 0xB1, 0xF, 0xF, false); break;    // xor 1
-      case 1: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, a), 0x4E, 0xF, 0xF, false); break;    // xor 2
-      case 2: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, a), 0x141, 0xF, 0xF, false); break;   // half-row mirror
-      default: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, a), 0x140, 0xF, 0xF, false); break;  // row mirror
+      case 0: r = __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false); break;    // quad_perm [1,0,3,2]
+      case 1: r = __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false); break;    // quad_perm [2,3,0,1]
+      case 2: r = __builtin_amdgcn_update_dpp(0, x, 0x141, 0xF, 0xF, false); break;   // half-row mirror
+      case 3: r = __builtin_amdgcn_update_dpp(0, x, 0x140, 0xF, 0xF, false); break;   // row mirror
+      case 4: r = __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false); break;   // row_bcast:15 -> rows 1, 3
+      default: r = __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false); break;  // row_bcast:31 -> rows 2, 3
     }
+    (void)row_mask;
     return __builtin_bit_cast(float, r);
   };
-  if (seg >= 2) v = v + dpp(v, 0);
-  if (seg >= 4) v = v + dpp(v, 1);
-  if (seg >= 8) v = v + dpp(v, 2);
-  if (seg >= 16) v = v + dpp(v, 3);
-  if (seg >= 32) {
-    const int lane = __lane_id();
-    const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
-    const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
-    const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
-    const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
-    const float lo = r0 + r1, hi = r2 + r3;
-    v = seg == 64 ? lo + hi : (lane < 32 ? lo : hi);
-  }
+  if (seg >= 2) v = v + shuffled(v, 0, 0xF);
+  if (seg >= 4) v = v + shuffled(v, 1, 0xF);
+  if (seg >= 8) v = v + shuffled(v, 2, 0xF);
+  if (seg >= 16) v = v + shuffled(v, 3, 0xF);
+  if (seg >= 32) v = v + shuffled(v, 4, 0xA);   // rows 1, 3: + the row before (lanes 31, 63 final for 32)
+  if (seg >= 64) v = v + shuffled(v, 5, 0xC);   // rows 2, 3: + lane 31 (lane 63 final for 64)
   return v;
 }
 
@@ -408,7 +424,16 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   constexpr bool kPreRec = kHostRanges || kPasses <= 2;
   if constexpr (!kHostRanges && kPreRec) load_rec_half(rec, MR, rec_index(kr), has_rec ? hh : 0);
 
-  // Set-up in LDS: x and the table.
+  // Set-up in LDS: the table first (it needs no loaded data, so it is built
+  // while x is still in flight), then x.
+  // One thread per code writes its 16 copies; at step q thread c writes copy
+  // (q + c) % 16, so the 16 lanes of an LDS pass hit 16 different bank
+  // quads.
+  for (int c = tid; c < 256; c += T) {
+    const uint4 e = lut_entry(c);
+#pragma unroll
+    for (int q = 0; q < kRep; ++q) reinterpret_cast<uint4*>(lut)[c * kRep + ((q + c) & (kRep - 1))] = e;
+  }
 #pragma unroll
   for (int q = 0; q < kXLoads; ++q) {
     // 8 halves: group i / 16, dwords 4 (i % 16) ..  Unconditional (threads
@@ -421,18 +446,10 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
     d[2] = xv[q].z;
     d[3] = xv[q].w;
   }
-  // One thread per code writes its 16 copies; at step q thread c writes copy
-  // (q + c) % 16, so the 16 lanes of an LDS pass hit 16 different bank
-  // quads.
-  for (int c = tid; c < 256; c += T) {
-    const uint4 e = lut_entry(c);
-#pragma unroll
-    for (int q = 0; q < kRep; ++q) reinterpret_cast<uint4*>(lut)[c * kRep + ((q + c) & (kRep - 1))] = e;
-  }
   __syncthreads();
 
   // This lane's activations.
-  uint32_t xr[kLaneBytes][3];
+  uint32_t xr[kXrRegs];
   load_xr(xr, xsw, g, h);
 
   // Plane 0, one row per pass: s0 * sum_i t0 x over each half-group, summed
@@ -448,7 +465,7 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
     asm volatile("" : "+v"(v));
     v = (active && row < nrb) ? v : 0.f;
     const float sum = segment_sum(v, seg);
-    if (in_rows && row < nrb && (sl & (seg - 1)) == 0) rowsum[row * segs + (sl >> 6)] = sum;
+    if (in_rows && row < nrb && (sl & (seg - 1)) == seg - 1) rowsum[row * segs + (sl >> 6)] = sum;
     __builtin_amdgcn_sched_barrier(0);   // keep passes apart: bounds the LUT reads in flight
   }
 
