@@ -361,13 +361,19 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   const uint32_t slot = (uint32_t)(tid & (kRep - 1)) << 4;
   const bool has_rec = M.nnz1 > 0;
 
-  // 1. Row pointers of this block: thread t < nrb reads the bounds of row t
-  //    (it sums that row's records at the end); without records x stands in
-  //    as a readable address.
+  // Loads, in the order their data is needed (each wait is then exact).
+  // 1. x.
+  uint4 xv[kXLoads];
+#pragma unroll
+  for (int q = 0; q < kXLoads; ++q) xv[q] = reinterpret_cast<const uint4*>(x)[min(tid + q * T, K / 8 - 1)];
+  // Keep the issue order: neither the optimiser nor the scheduler may move
+  // loads across these points (no instruction emitted).
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  // 2. The block's record range: from the arguments with host ranges, else
+  //    its first and last row pointers.  Without records x stands in as a
+  //    readable address.
   const int* rpb = has_rec ? M.rowptr1 + row_begin : reinterpret_cast<const int*>(x);
-  const int tr = has_rec ? min(tid, nrb - 1) : 0;
-  const int rpa = rpb[tr];
-  const int rpz = rpb[has_rec ? tr + 1 : 0];
   int k0, k1;
   if constexpr (kHostRanges) {
     k0 = hk0;
@@ -395,14 +401,6 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   // Threads past the block's records reload its last record (no extra
   // cache lines); the values are ignored.
   auto rec_index = [&](int k) -> uint32_t { return (uint32_t)max(min(k, min(max(k1 - 1, k0), kmax)), 0); };
-  // 2. x.
-  uint4 xv[kXLoads];
-#pragma unroll
-  for (int q = 0; q < kXLoads; ++q) xv[q] = reinterpret_cast<const uint4*>(x)[min(tid + q * T, K / 8 - 1)];
-  // Keep the issue order = the order of need: neither the optimiser nor the
-  // scheduler may move loads across these points (no instruction emitted).
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_sched_barrier(0);
   // 3. With host ranges the first sweep of records needs no row pointer.
   if constexpr (kHostRanges) load_rec_half(rec, MR, rec_index(kr), has_rec ? hh : 0);
   asm volatile("" ::: "memory");
@@ -419,7 +417,14 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   }
   asm volatile("" ::: "memory");
   __builtin_amdgcn_sched_barrier(0);
-  // 5. Without host ranges: the first sweep of records once the range is
+  // 5. Thread t < nrb: the bounds of row t (it adds that row's records at
+  //    the end).
+  const int tr = has_rec ? min(tid, nrb - 1) : 0;
+  const int rpa = rpb[tr];
+  const int rpz = rpb[has_rec ? tr + 1 : 0];
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  // 6. Without host ranges: the first sweep of records once the range is
   //    known, when few passes leave registers to spare (else after plane 0).
   constexpr bool kPreRec = kHostRanges || kPasses <= 2;
   if constexpr (!kHostRanges && kPreRec) load_rec_half(rec, MR, rec_index(kr), has_rec ? hh : 0);
