@@ -383,8 +383,8 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
     k1 = rpb[has_rec ? nrb : 0];
   }
   // Record halves: two consecutive threads per record, so that the record
-  // work occupies as few waves as possible (an LDS instruction costs the
-  // same however few of its lanes are active).
+  // work occupies as few waves as possible (the record code costs a wave
+  // the same time however few of its lanes have a record).
   const int hh = tid & 1;
   const int kr = k0 + (tid >> 1);
   const int per_sweep = T >> 1;
@@ -490,8 +490,18 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
     float a = rowsum[tid * segs];
     for (int c = 1; c < segs; ++c) a += rowsum[tid * segs + c];
     if (has_rec) {
+      // Four records per step, loads first (absent ones add +0).
       const int kb = max(rpa, k0), ke = min(min(rpz, k1), k0 + rec_cap);
-      for (int k = kb; k < ke; ++k) a += recval[2 * (k - k0)] + recval[2 * (k - k0) + 1];
+      for (int k = kb; k < ke; k += 4) {
+        float v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int kk = min(k + u, ke - 1) - k0;
+          v[u] = recval[2 * kk] + recval[2 * kk + 1];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) a += k + u < ke ? v[u] : 0.f;
+      }
     }
     store_y(yp, row_begin + tid, a, out_f32);
   }
