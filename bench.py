@@ -15,6 +15,8 @@ timed region on the launch stream over the launches it holds) and the CPU
 oracle timed on a bounded sample.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--layers 36]
+    python bench.py --extra     # also: small batch, codec, and the 4096 x 2560
+                                # comparison with dense fp16 (one JSON line each)
 """
 
 import argparse
@@ -120,6 +122,111 @@ def cpu_baseline(layers=2):
                       f"host has {os.cpu_count()} logical CPUs"}
 
 
+def graph_time_us(calls, reps=3):
+    """Median over `reps` replays of a HIP graph holding `calls` (a list of
+    zero-argument launches), per call, in microseconds."""
+    import torch
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        for c in calls:
+            c()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for c in calls:
+            c()
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps + 1):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            a.record(stream)
+            g.replay()
+            b.record(stream)
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b) * 1e3 / len(calls))
+    return sorted(times[1:])[reps // 2]
+
+
+def copies_of(mat, n):
+    """n device copies of a packed linear (same values, distinct buffers), so
+    that rotating over them streams from HBM."""
+    import dataclasses
+    out = []
+    for _ in range(n):
+        kw = {f.name: getattr(mat, f.name) for f in dataclasses.fields(mat)}
+        for k, v in kw.items():
+            if k != "rowptr1_host" and hasattr(v, "clone"):
+                kw[k] = v.clone()
+        out.append(type(mat)(**kw))
+    return out
+
+
+def extra_suite(dev):
+    """Small batch (MFMA path), codec throughput, and the paper's 4096 x 2560
+    comparison (dense fp16 GEMV, packed GEMV, unpack + dense GEMV)."""
+    import torch
+
+    from paper_2609_09240_amd import synth, tq
+    lines = []
+    ring = 32   # copies per measurement: > 256 MB for the 12 MB matrices
+
+    # Small batch on the MLP shapes.
+    for name in ("gate", "down"):
+        inp = synth.projection(name, layer=0, cfg=4)
+        base = tq.PackedLinear.from_inputs(inp, dev)
+        mats = copies_of(base, ring)
+        for B in (1, 4, 16, 64):
+            X = torch.from_numpy(synth.stage_activations(synth.STAGE_OF[name], layer=0, cfg=4, batch=B)).to(dev)
+            Y = torch.empty(B, inp.n_out, dtype=torch.float16, device=dev)
+            calls = [lambda m=m: tq.tq_gemm_smallbatch(m, X, Y=Y, stream=torch.cuda.current_stream()) for m in mats]
+            us = graph_time_us(calls)
+            nbytes = base.nbytes() + 2 * B * (inp.n_in + inp.n_out)
+            tflops = 2.0 * B * inp.n_out * inp.n_in / (us * 1e-6) / 1e12
+            lines.append({"bench": "smallbatch", "matrix": f"{name} {inp.n_out}x{inp.n_in}", "batch": B,
+                          "us": round(us, 2), "GBps": round(nbytes / us / 1e3, 1), "TFLOPs": round(tflops, 2),
+                          "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4),
+                          "mfma_fp16_frac": round(tflops / 2500.0, 4)})
+        del mats, base
+
+    # Codec on the gate projection (plane 0).
+    inp = synth.projection("gate", layer=0, cfg=4)
+    trits = torch.from_numpy(inp.t0.reshape(-1, 128)).to(dev)
+    codes = tq.tq_pack(trits)
+    ng = trits.shape[0]
+    us = graph_time_us([lambda: tq.tq_pack(trits, codes=codes, stream=torch.cuda.current_stream())] * 8)
+    lines.append({"bench": "tq_pack", "groups": ng, "us": round(us, 2), "GBps": round((128 + 26) * ng / us / 1e3, 1)})
+    out_t = torch.empty_like(trits)
+    us = graph_time_us([lambda: tq.tq_unpack(codes, ng, trits=out_t, stream=torch.cuda.current_stream())] * 8)
+    lines.append({"bench": "tq_unpack", "groups": ng, "us": round(us, 2), "GBps": round((128 + 26) * ng / us / 1e3, 1)})
+    mat = tq.PackedLinear.from_inputs(inp, dev)
+    w = torch.empty(inp.n_out, inp.n_in, dtype=torch.float16, device=dev)
+    us = graph_time_us([lambda: tq.tq_unpack_fp16(mat, w=w, stream=torch.cuda.current_stream())] * 8)
+    nb = mat.nbytes() + 2 * inp.n_out * inp.n_in
+    lines.append({"bench": "tq_unpack_fp16", "matrix": f"gate {inp.n_out}x{inp.n_in}", "us": round(us, 2),
+                  "GBps": round(nb / us / 1e3, 1)})
+    del trits, codes, out_t, mat, w
+
+    # The paper's microbenchmark shape (out 4096, in 2560), cold caches.
+    inp = synth.linear(4096, 2560, synth.TWO_PLANE, (9, 4096, 2560, 0))
+    x = torch.from_numpy(synth.activations(2560, (9, 4096, 2560, 1))).to(dev)
+    base = tq.PackedLinear.from_inputs(inp, dev)
+    mats = copies_of(base, 256)
+    dense = [tq.tq_unpack_fp16(m) for m in mats[:64]]
+    torch.cuda.synchronize()
+    y = torch.empty(4096, dtype=torch.float16, device=dev)
+    t_dense = graph_time_us([lambda W=W: torch.mv(W, x, out=y) for W in dense])
+    t_packed = graph_time_us([lambda m=m: tq.tq_gemv(m, x, y=y, stream=torch.cuda.current_stream()) for m in mats])
+    scratch = torch.empty(4096, 2560, dtype=torch.float16, device=dev)
+    t_unpack = graph_time_us([lambda m=m: (tq.tq_unpack_fp16(m, w=scratch, stream=torch.cuda.current_stream()),
+                                           torch.mv(scratch, x, out=y)) for m in mats[:64]])
+    lines.append({"bench": "paper_shape_4096x2560", "dense_fp16_mv_us": round(t_dense, 2),
+                  "packed_gemv_us": round(t_packed, 2), "unpack_fp16_plus_mv_us": round(t_unpack, 2),
+                  "packed_vs_dense": round(t_packed / t_dense, 3), "unpack_plus_mv_vs_dense": round(t_unpack / t_dense, 3),
+                  "packed_bytes": base.nbytes(), "dense_bytes": 2 * 4096 * 2560})
+    return lines
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -127,6 +234,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--layers", type=int, default=36)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--extra", action="store_true",
+                    help="also print small-batch, codec and 4096 x 2560 comparison lines")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the packed GEMV path is single-device; "
@@ -239,6 +348,11 @@ def main():
         log("timing the CPU oracle on a bounded sample ...")
         result["cpu_baseline"] = cpu_baseline()
     print(json.dumps(result), flush=True)
+    if args.extra:
+        del graph, outs, launches, mats, xs
+        torch.cuda.empty_cache()
+        for line in extra_suite(dev):
+            print(json.dumps(line), flush=True)
 
 
 if __name__ == "__main__":
