@@ -189,23 +189,27 @@ def extra_suite(dev):
                           "mfma_fp16_frac": round(tflops / 2500.0, 4)})
         del mats, base
 
-    # Codec on the gate projection (plane 0).
+    # Codec on the gate projection (plane 0), rotating over 6 copies (>256 MiB,
+    # so each call streams from HBM rather than the last-level cache).
     inp = synth.projection("gate", layer=0, cfg=4)
-    trits = torch.from_numpy(inp.t0.reshape(-1, 128)).to(dev)
-    codes = tq.tq_pack(trits)
-    ng = trits.shape[0]
-    us = graph_time_us([lambda: tq.tq_pack(trits, codes=codes, stream=torch.cuda.current_stream())] * 8)
+    trits = [torch.from_numpy(inp.t0.reshape(-1, 128)).to(dev) for _ in range(6)]
+    codes = [tq.tq_pack(t) for t in trits]
+    ng = trits[0].shape[0]
+    us = graph_time_us([lambda i=i: tq.tq_pack(trits[i], codes=codes[i]) for i in range(6)] * 2)
     lines.append({"bench": "tq_pack", "groups": ng, "us": round(us, 2), "GBps": round((128 + 26) * ng / us / 1e3, 1)})
-    out_t = torch.empty_like(trits)
-    us = graph_time_us([lambda: tq.tq_unpack(codes, ng, trits=out_t, stream=torch.cuda.current_stream())] * 8)
+    us = graph_time_us([lambda i=i: tq.tq_unpack(codes[i], ng, trits=trits[5 - i]) for i in range(6)] * 2)
     lines.append({"bench": "tq_unpack", "groups": ng, "us": round(us, 2), "GBps": round((128 + 26) * ng / us / 1e3, 1)})
-    mat = tq.PackedLinear.from_inputs(inp, dev)
-    w = torch.empty(inp.n_out, inp.n_in, dtype=torch.float16, device=dev)
-    us = graph_time_us([lambda: tq.tq_unpack_fp16(mat, w=w, stream=torch.cuda.current_stream())] * 8)
-    nb = mat.nbytes() + 2 * inp.n_out * inp.n_in
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    us = graph_time_us([lambda i=i: tq.tq_validate(codes[i], ng, d_err=err) for i in range(6)] * 2)
+    lines.append({"bench": "tq_validate", "groups": ng, "us": round(us, 2), "GBps": round(26 * ng / us / 1e3, 1)})
+    del trits, codes
+    mats = [tq.PackedLinear.from_inputs(inp, dev) for _ in range(2)]
+    ws = [torch.empty(inp.n_out, inp.n_in, dtype=torch.float16, device=dev) for _ in range(3)]
+    us = graph_time_us([lambda i=i: tq.tq_unpack_fp16(mats[i % 2], w=ws[i % 3]) for i in range(6)] * 2)
+    nb = mats[0].nbytes() + 2 * inp.n_out * inp.n_in
     lines.append({"bench": "tq_unpack_fp16", "matrix": f"gate {inp.n_out}x{inp.n_in}", "us": round(us, 2),
                   "GBps": round(nb / us / 1e3, 1)})
-    del trits, codes, out_t, mat, w
+    del mats, ws
 
     # The paper's microbenchmark shape (out 4096, in 2560), cold caches.
     inp = synth.linear(4096, 2560, synth.TWO_PLANE, (9, 4096, 2560, 0))

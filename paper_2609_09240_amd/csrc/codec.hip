@@ -6,22 +6,192 @@
 // sum_i (t + 1) 3^i; bytes 0..23 of group f sit at 24 f, bytes 24..25 at
 // 24 n + 2 f (the split layout declared in tq.h).
 //
-// These kernels move a few bytes per thread and are HBM-bound; each thread
-// owns one code byte (pack, unpack, validate) or one 16-byte run of the
-// dense output (unpack_fp16), so consecutive lanes touch consecutive bytes.
+// All of these are HBM-bound streams.  Pack and unpack give each group three
+// threads (part p owns main code bytes 8p..8p+7, part 2 also the two tail
+// bytes), so every thread moves 8 code bytes and 40-48 trit bytes with vector
+// loads and stores and consecutive lanes touch consecutive memory.  A trit
+// buffer that is not 16-byte aligned takes a one-byte-per-thread kernel.
+// Validate reads the code buffer in flat 8-byte chunks.  The fp16
+// dequantisation stages one row's codes, scales and plane-1 record table in
+// LDS and writes the row with 16-byte stores.
 
 #include "tq_internal.h"
 
 namespace tq {
 namespace {
 
-constexpr int kThreads = 256;
 constexpr int64_t kMaxBlocks = 1 << 16;
 
-__host__ __device__ inline int64_t grid_for(int64_t work) {
-  int64_t b = (work + kThreads - 1) / kThreads;
-  return b < 1 ? 1 : (b > kMaxBlocks ? kMaxBlocks : b);
+constexpr int kPartThreads = 192;   // three threads per group
+constexpr int kPartGroups = 64;     // groups per workgroup pass
+constexpr int kPartMaxBlocks = 2048;
+
+constexpr int kByteThreads = 256;
+
+constexpr int kRowThreads = 64;     // fp16 dequantisation: one row per workgroup pass
+constexpr int kRowMaxBlocks = 8192;
+
+inline int64_t clamp_blocks(int64_t b, int64_t cap) { return b < 1 ? 1 : (b > cap ? cap : b); }
+
+// Adds the wave's number of bad bytes to *d_err: one vector atomic per wave
+// that saw any.  Every lane of the wave must call it.
+__device__ inline void count_errors(int32_t* d_err, int nbad) {
+  if (d_err == nullptr || __ballot(nbad != 0) == 0) return;
+  for (int off = 32; off > 0; off >>= 1) nbad += __shfl_xor(nbad, off);
+  if (__lane_id() == 0) atomicAdd(d_err, nbad);
 }
+
+// ---------------------------------------------------------------------------
+// Pack.
+// ---------------------------------------------------------------------------
+
+// Signed trit byte b of a little-endian word array.
+__device__ inline int trit_at(const uint32_t* w, int b) { return (int)(int8_t)(w[b >> 2] >> (8 * (b & 3))); }
+
+// Code of the trits w[b .. b+nt-1] (digits nt..4 are pad zeros, digit 1);
+// 0xFF and one bad byte if any trit is outside {-1, 0, +1}.
+__device__ inline uint32_t encode(const uint32_t* w, int b, int nt, int& nbad) {
+  uint32_t code = 0, top = 0;
+#pragma unroll
+  for (int k = 4; k >= 0; --k) {
+    const uint32_t u = k < nt ? (uint32_t)(trit_at(w, b + k) + 1) : 1u;
+    top = u > top ? u : top;
+    code = code * 3u + u;
+  }
+  const bool bad = top > 2u;
+  nbad += bad;
+  return bad ? 0xFFu : code;
+}
+
+__global__ void __launch_bounds__(kPartThreads) pack_kernel(const int8_t* __restrict__ trits, int64_t n,
+                                                            uint8_t* __restrict__ codes, int32_t* d_err) {
+  const int part = threadIdx.x % 3;
+  const int slot = threadIdx.x / 3;
+  const int first = part == 0 ? 0 : (part == 1 ? 32 : 80);   // first trit loaded (16-byte aligned)
+  for (int64_t base = (int64_t)blockIdx.x * kPartGroups; base < n; base += (int64_t)gridDim.x * kPartGroups) {
+    const int64_t f = base + slot;
+    int nbad = 0;
+    if (f < n) {
+      const uint4* src = reinterpret_cast<const uint4*>(trits + f * kGroup + first);
+      const uint4 a = src[0], b = src[1], c = src[2];
+      const uint32_t raw[12] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w, c.x, c.y, c.z, c.w};
+      // Trit 40*part at w[0]: part 1 loaded from trit 32, two words early.
+      uint32_t w[12];
+#pragma unroll
+      for (int d = 0; d < 10; ++d) w[d] = part == 1 ? raw[d + 2] : raw[d];
+      w[10] = raw[10];
+      w[11] = raw[11];
+      uint32_t out[2] = {0u, 0u};
+#pragma unroll
+      for (int i = 0; i < 8; ++i) out[i >> 2] |= encode(w, 5 * i, 5, nbad) << (8 * (i & 3));
+      *reinterpret_cast<uint2*>(codes + 24 * f + 8 * part) = make_uint2(out[0], out[1]);
+      if (part == 2) {   // bytes 24 and 25: trits 120..124 and 125..127
+        const uint32_t c24 = encode(w, 40, 5, nbad), c25 = encode(w, 45, 3, nbad);
+        *reinterpret_cast<uint16_t*>(codes + (int64_t)kMainBytes * n + 2 * f) = (uint16_t)(c24 | (c25 << 8));
+      }
+    }
+    count_errors(d_err, nbad);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Unpack.
+// ---------------------------------------------------------------------------
+
+// The five trit bytes (t as int8) of a code, bytes 0..3 in .x and 4 in .y;
+// codes above 242 decode to five zeros.  (c * 171) >> 9 == c / 3 for c < 256.
+__device__ inline uint2 trit_bytes(int c) {
+  if (c > 242) c = 121;
+  uint32_t lo = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int q = (c * 171) >> 9;
+    lo |= (uint32_t)(uint8_t)(c - 3 * q - 1) << (8 * k);
+    c = q;
+  }
+  return make_uint2(lo, (uint32_t)(uint8_t)(c - 1));
+}
+
+// ORs the trit bytes e of one code into out[] at byte offset o (bytes past
+// `limit` dropped).
+template <int o, int limit>
+__device__ inline void place(uint32_t* out, uint2 e) {
+  constexpr int d = o >> 2, s = 8 * (o & 3);
+  out[d] |= e.x << s;
+  if constexpr (d + 1 < limit / 4) {
+    if constexpr (s == 0) out[d + 1] |= e.y;
+    else out[d + 1] |= (e.x >> (32 - s)) | (e.y << s);
+  }
+}
+
+__global__ void __launch_bounds__(kPartThreads) unpack_kernel(const uint8_t* __restrict__ codes, int64_t n,
+                                                              int8_t* __restrict__ trits, int32_t* d_err) {
+  __shared__ uint2 table[256];
+  // The pass's 64 groups of trits, written back with 16-byte lanes over
+  // consecutive addresses (per-thread stores would cut every line in pieces).
+  __shared__ uint4 tile[kPartGroups * kGroup / 16];
+  for (int c = threadIdx.x; c < 256; c += kPartThreads) table[c] = trit_bytes(c);
+  __syncthreads();
+  const int part = threadIdx.x % 3;
+  const int slot = threadIdx.x / 3;
+  uint8_t* tile_b = reinterpret_cast<uint8_t*>(tile) + slot * kGroup;
+  for (int64_t base = (int64_t)blockIdx.x * kPartGroups; base < n; base += (int64_t)gridDim.x * kPartGroups) {
+    const int64_t f = base + slot;
+    int nbad = 0;
+    if (f < n) {
+      const uint2 cw = *reinterpret_cast<const uint2*>(codes + 24 * f + 8 * part);
+      uint32_t tail = 0;
+      if (part == 2) tail = *reinterpret_cast<const uint16_t*>(codes + (int64_t)kMainBytes * n + 2 * f);
+      uint32_t cb[10];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        cb[i] = (cw.x >> (8 * i)) & 0xFFu;
+        cb[4 + i] = (cw.y >> (8 * i)) & 0xFFu;
+      }
+      cb[8] = tail & 0xFFu;
+      cb[9] = tail >> 8;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) nbad += cb[i] > 242u;
+      if (part == 2) nbad += (cb[8] > 242u) + (cb[9] > 242u);
+      uint32_t out[12] = {};
+      place<0, 48>(out, table[cb[0]]);
+      place<5, 48>(out, table[cb[1]]);
+      place<10, 48>(out, table[cb[2]]);
+      place<15, 48>(out, table[cb[3]]);
+      place<20, 48>(out, table[cb[4]]);
+      place<25, 48>(out, table[cb[5]]);
+      place<30, 48>(out, table[cb[6]]);
+      place<35, 48>(out, table[cb[7]]);
+      if (part == 1) {   // trits 40..79
+        *reinterpret_cast<uint2*>(tile_b + 40) = make_uint2(out[0], out[1]);
+        *reinterpret_cast<uint4*>(tile_b + 48) = make_uint4(out[2], out[3], out[4], out[5]);
+        *reinterpret_cast<uint4*>(tile_b + 64) = make_uint4(out[6], out[7], out[8], out[9]);
+      } else if (part == 0) {   // trits 0..39
+        *reinterpret_cast<uint4*>(tile_b) = make_uint4(out[0], out[1], out[2], out[3]);
+        *reinterpret_cast<uint4*>(tile_b + 16) = make_uint4(out[4], out[5], out[6], out[7]);
+        *reinterpret_cast<uint2*>(tile_b + 32) = make_uint2(out[8], out[9]);
+      } else {   // trits 80..127: bytes 24 (5 trits) and 25 (3 trits) fill 40..47
+        place<40, 48>(out, table[cb[8]]);
+        place<45, 48>(out, table[cb[9]]);
+        *reinterpret_cast<uint4*>(tile_b + 80) = make_uint4(out[0], out[1], out[2], out[3]);
+        *reinterpret_cast<uint4*>(tile_b + 96) = make_uint4(out[4], out[5], out[6], out[7]);
+        *reinterpret_cast<uint4*>(tile_b + 112) = make_uint4(out[8], out[9], out[10], out[11]);
+      }
+    }
+    count_errors(d_err, nbad);
+    __syncthreads();
+    const int64_t left = n - base;
+    const int chunks = (int)(left < kPartGroups ? left : kPartGroups) * (kGroup / 16);
+    uint4* dst = reinterpret_cast<uint4*>(trits + base * kGroup);
+    for (int i = threadIdx.x; i < chunks; i += kPartThreads) dst[i] = tile[i];
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// One-byte-per-thread pack and unpack, for trit buffers that are not 16-byte
+// aligned.
+// ---------------------------------------------------------------------------
 
 // Group index and byte index of storage position `pos` in a buffer of n groups.
 __device__ inline void locate(int64_t pos, int64_t n, int64_t& f, int& j) {
@@ -36,33 +206,19 @@ __device__ inline void locate(int64_t pos, int64_t n, int64_t& f, int& j) {
   }
 }
 
-// Storage offset of byte j of group f in a buffer of n groups.
-__device__ inline int64_t byte_offset(int64_t f, int j, int64_t n) {
-  return j < kMainBytes ? f * kMainBytes + j : (int64_t)kMainBytes * n + 2 * f + (j - kMainBytes);
-}
-
-__device__ inline void count_error(int32_t* d_err, bool bad) {
-  // One atomic per wave that saw errors (vector memory atomic).
-  uint64_t m = __ballot(bad);
-  if (m != 0 && d_err != nullptr) {
-    int lane = __lane_id();
-    int first = __builtin_ctzll(m);
-    if (lane == first) atomicAdd(d_err, (int32_t)__popcll(m));
-  }
-}
-
-__global__ void __launch_bounds__(kThreads) pack_kernel(const int8_t* __restrict__ trits, int64_t n,
-                                                        uint8_t* __restrict__ codes, int32_t* d_err) {
+__global__ void __launch_bounds__(kByteThreads) pack_bytes_kernel(const int8_t* __restrict__ trits, int64_t n,
+                                                                  uint8_t* __restrict__ codes, int32_t* d_err) {
   const int64_t total = (int64_t)kGroupBytes * n;
-  const int64_t stride = (int64_t)gridDim.x * kThreads;
-  for (int64_t base = (int64_t)blockIdx.x * kThreads; base < total; base += stride) {
+  const int64_t stride = (int64_t)gridDim.x * kByteThreads;
+  for (int64_t base = (int64_t)blockIdx.x * kByteThreads; base < total; base += stride) {
     int64_t pos = base + threadIdx.x;
-    bool bad = false;
+    int nbad = 0;
     if (pos < total) {
       int64_t f;
       int j;
       locate(pos, n, f, j);
       const int8_t* t = trits + f * kGroup + 5 * j;
+      bool bad = false;
       int code = 0, mul = 1;
 #pragma unroll
       for (int i = 0; i < 5; ++i) {
@@ -72,25 +228,26 @@ __global__ void __launch_bounds__(kThreads) pack_kernel(const int8_t* __restrict
         mul *= 3;
       }
       codes[pos] = bad ? (uint8_t)0xFF : (uint8_t)code;
+      nbad = bad;
     }
-    count_error(d_err, bad);
+    count_errors(d_err, nbad);
   }
 }
 
-__global__ void __launch_bounds__(kThreads) unpack_kernel(const uint8_t* __restrict__ codes, int64_t n,
-                                                          int8_t* __restrict__ trits, int32_t* d_err) {
+__global__ void __launch_bounds__(kByteThreads) unpack_bytes_kernel(const uint8_t* __restrict__ codes, int64_t n,
+                                                                    int8_t* __restrict__ trits, int32_t* d_err) {
   const int64_t total = (int64_t)kGroupBytes * n;
-  const int64_t stride = (int64_t)gridDim.x * kThreads;
-  for (int64_t base = (int64_t)blockIdx.x * kThreads; base < total; base += stride) {
+  const int64_t stride = (int64_t)gridDim.x * kByteThreads;
+  for (int64_t base = (int64_t)blockIdx.x * kByteThreads; base < total; base += stride) {
     int64_t pos = base + threadIdx.x;
-    bool bad = false;
+    int nbad = 0;
     if (pos < total) {
       int64_t f;
       int j;
       locate(pos, n, f, j);
       int c = codes[pos];
-      bad = c > 242;
-      if (bad) c = 121;                      // five zero trits
+      nbad = c > 242;
+      if (nbad) c = 121;                      // five zero trits
       int8_t* t = trits + f * kGroup + 5 * j;
 #pragma unroll
       for (int i = 0; i < 5; ++i) {
@@ -98,117 +255,293 @@ __global__ void __launch_bounds__(kThreads) unpack_kernel(const uint8_t* __restr
         c /= 3;
       }
     }
-    count_error(d_err, bad);
+    count_errors(d_err, nbad);
   }
 }
 
-__global__ void __launch_bounds__(kThreads) validate_kernel(const uint8_t* __restrict__ codes, int64_t n,
-                                                            int32_t* d_err) {
+// ---------------------------------------------------------------------------
+// Validate: flat 8-byte chunks.  The main region (24 n bytes) is a multiple
+// of 8, so a chunk is all main bytes or all tail bytes; in the tail, odd
+// bytes are byte 25, whose pad digits 3 and 4 must be 1 (108 <= c <= 134).
+// ---------------------------------------------------------------------------
+
+__device__ inline int bad_main(uint32_t w) {
+  int nb = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) nb += ((w >> (8 * i)) & 0xFFu) > 242u;
+  return nb;
+}
+
+__device__ inline int bad_tail(uint32_t w) {
+  int nb = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t c = (w >> (8 * i)) & 0xFFu;
+    nb += (i & 1) ? (c < 108u || c > 134u) : (c > 242u);
+  }
+  return nb;
+}
+
+__global__ void __launch_bounds__(kByteThreads) validate_kernel(const uint8_t* __restrict__ codes, int64_t n,
+                                                                int32_t* d_err) {
   const int64_t total = (int64_t)kGroupBytes * n;
-  const int64_t stride = (int64_t)gridDim.x * kThreads;
-  for (int64_t base = (int64_t)blockIdx.x * kThreads; base < total; base += stride) {
-    int64_t pos = base + threadIdx.x;
-    bool bad = false;
-    if (pos < total) {
-      int64_t f;
-      int j;
-      locate(pos, n, f, j);
-      int c = codes[pos];
-      bad = c > 242;
-      if (!bad && j == kGroupBytes - 1) bad = (c / 27) != 4;   // pad digits 3, 4 must be 1
+  const int64_t main_bytes = (int64_t)kMainBytes * n;
+  const int64_t chunks = (total + 7) >> 3;
+  const int64_t stride = (int64_t)gridDim.x * kByteThreads;
+  for (int64_t base = (int64_t)blockIdx.x * kByteThreads; base < chunks; base += stride) {
+    const int64_t i = base + threadIdx.x;
+    int nbad = 0;
+    if (i < chunks) {
+      const int64_t pos = 8 * i;
+      uint32_t w0, w1;
+      if (pos + 8 <= total) {
+        const uint2 v = *reinterpret_cast<const uint2*>(codes + pos);
+        w0 = v.x;
+        w1 = v.y;
+      } else {   // last, partial chunk (tail region): missing bytes read as 121, valid everywhere
+        uint32_t b[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) b[k] = pos + k < total ? codes[pos + k] : 121u;
+        w0 = b[0] | (b[1] << 8) | (b[2] << 16) | (b[3] << 24);
+        w1 = b[4] | (b[5] << 8) | (b[6] << 16) | (b[7] << 24);
+      }
+      nbad = pos < main_bytes ? bad_main(w0) + bad_main(w1) : bad_tail(w0) + bad_tail(w1);
     }
-    count_error(d_err, bad);
+    count_errors(d_err, nbad);
   }
 }
 
-// Record index of (row r, group g) in the CSR of plane 1, or -1.
-__device__ inline int64_t find_record(const MatDev& m, int64_t r, int g) {
-  if (m.nnz1 == 0) return -1;
-  int64_t lo = m.rowptr1[r], hi = m.rowptr1[r + 1];
-  while (lo < hi) {
-    int64_t mid = (lo + hi) >> 1;
-    if ((int)m.gidx1[mid] < g) lo = mid + 1; else hi = mid;
+// ---------------------------------------------------------------------------
+// Dense fp16 dequantisation.
+// ---------------------------------------------------------------------------
+
+// Base-3 digits of a code in 2-bit fields (digit k at bits 2k, 2k+1); codes
+// above 242 read as 121 (the kernel's output for invalid codes is unspecified).
+__device__ inline uint32_t digit_fields(int c) {
+  if (c > 242) c = 121;
+  uint32_t v = 0;
+#pragma unroll
+  for (int k = 0; k < 5; ++k) {
+    const int q = (c * 171) >> 9;
+    v |= (uint32_t)(c - 3 * q) << (2 * k);
+    c = q;
   }
-  return (lo < m.rowptr1[r + 1] && (int)m.gidx1[lo] == g) ? lo : -1;
+  return v;
 }
 
-__device__ inline float half_bits_to_float(uint16_t b) {
-  return (float)__builtin_bit_cast(_Float16, b);
+__device__ inline float half_bits_to_float(uint32_t b) { return (float)__builtin_bit_cast(_Float16, (uint16_t)b); }
+
+__device__ inline uint32_t float_to_half_bits(float a) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)a);   // nearest-even
 }
 
-// One thread writes 8 consecutive fp16 weights (16 bytes) of one group.
-__global__ void __launch_bounds__(kThreads) unpack_fp16_kernel(MatDev m, uint16_t* __restrict__ w) {
-  const int64_t n = (int64_t)m.n_out * m.n_groups;
-  const int64_t total = n * 16;
-  const int64_t stride = (int64_t)gridDim.x * kThreads;
-  for (int64_t id = (int64_t)blockIdx.x * kThreads + threadIdx.x; id < total; id += stride) {
-    const int64_t f = id >> 4;
-    const int c = (int)(id & 15);
-    const int64_t r = f / m.n_groups;
-    const int g = (int)(f - r * m.n_groups);
-    const int64_t k = find_record(m, r, g);
-    const float s0 = half_bits_to_float(m.scale0[f]);
-    float mu = 0.f, s1 = 0.f;
-    if (k >= 0) {
-      mu = half_bits_to_float(m.offset1[k]);
-      s1 = half_bits_to_float(m.scale1[k]);
+// v_perm selectors for two weights of one plane with digits (u_a, u_b) =
+// (e & 3, e >> 2), picking from S = s0 | (s0 ^ 0x8000) << 16: digit 0 (t = -1)
+// takes bytes 0 and 3 (-s0), digit 2 (t = +1) bytes 0 and 1 (s0), digit 1
+// (t = 0) selector 12, a zero byte.
+__device__ inline uint32_t pair_selector(int e) {
+  const uint32_t sel[4] = {0x0300u, 0x0C0Cu, 0x0100u, 0x0C0Cu};
+  return sel[e & 3] | (sel[(e >> 2) & 3] << 16);
+}
+
+// One wave per workgroup, so the LDS writes of a row (table reset, record
+// scatter) take effect in program order without barriers between them.
+// Dynamic LDS, 70 bytes per group of the row:
+//   grp_s  [8 G] words: per group bytes 0..23, 24..25, six zero bytes
+//   rcd_s  [8 G] words: the same for the row's plane-1 records (slot q =
+//          record k - rowptr1[r]), with mu | s1 << 16 in the last word
+//   rec_s  [G]   record slot of each group, or -1
+//   scale_s[G]   s0
+constexpr int kCodeBatch = 12;   // code words loaded per thread before one wait (6 G <= 768 in one batch)
+constexpr int kGroupBatch = 4;   // G <= 256 tails and scales per thread in one batch
+
+__global__ void __launch_bounds__(kRowThreads) unpack_fp16_kernel(MatDev m, uint16_t* __restrict__ w) {
+  static_assert(kRowThreads == 64, "the row staging relies on a one-wave workgroup");
+  __shared__ uint32_t digits[256];
+  __shared__ uint32_t selector[16];
+  extern __shared__ uint32_t dyn[];
+  const int G = m.n_groups;
+  uint32_t* grp_s = dyn;
+  uint32_t* rcd_s = dyn + 8 * G;
+  int32_t* rec_s = reinterpret_cast<int32_t*>(dyn + 16 * G);
+  uint16_t* scale_s = reinterpret_cast<uint16_t*>(rec_s + G);
+  const int tid = threadIdx.x;
+  for (int c = tid; c < 256; c += kRowThreads) digits[c] = digit_fields(c);
+  if (tid < 16) selector[tid] = pair_selector(tid);
+  const int64_t n = (int64_t)m.n_out * G;
+  for (int r = blockIdx.x; r < m.n_out; r += gridDim.x) {
+    const int64_t f0 = (int64_t)r * G;
+    int k0 = 0, R = 0;
+    if (m.nnz1 > 0) {
+      k0 = m.rowptr1[r];
+      R = m.rowptr1[r + 1] - k0;
+      R = R < G ? R : G;   // a valid row has at most G records
     }
-    const int p0 = 8 * c;
-    const int j0 = p0 / 5;
-    int b0[3], b1[3];
+    // Plane-0 bytes of the row: 6 G words from 24 f0, then 2 G tail bytes.
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(m.codes0 + 24 * f0);
+    const uint16_t* tsrc = reinterpret_cast<const uint16_t*>(m.codes0 + (int64_t)kMainBytes * n) + f0;
+    uint32_t tl[kGroupBatch], sc[kGroupBatch];
 #pragma unroll
-    for (int q = 0; q < 3; ++q) {
-      int j = j0 + q;
-      j = j < kGroupBytes ? j : kGroupBytes - 1;
-      b0[q] = m.codes0[byte_offset(f, j, n)];
-      b1[q] = k >= 0 ? m.codes1[byte_offset(k, j, m.nnz1)] : 121;
+    for (int u = 0; u < kGroupBatch; ++u) {
+      const int g = tid + u * kRowThreads;
+      tl[u] = g < G ? tsrc[g] : 0u;
+      sc[u] = g < G ? m.scale0[f0 + g] : 0u;
     }
-    uint32_t outw[4];
+    for (int i0 = 0; i0 < 6 * G; i0 += kCodeBatch * kRowThreads) {
+      uint32_t v[kCodeBatch];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int p = p0 + e;
-      const int q = p / 5 - j0;
-      const int d = p % 5;
-      int c0 = b0[q], c1 = b1[q];
-      for (int i = 0; i < d; ++i) { c0 /= 3; c1 /= 3; }
-      const float t0 = (float)(c0 % 3 - 1);
-      const float t1 = (float)(c1 % 3 - 1);
-      float a = 0.0f;
-      if (k >= 0) a = a + mu;
-      a = a + s0 * t0;                  // s0*t0 is exact: one rounding
-      if (k >= 0) a = a + s1 * t1;
-      const uint16_t h = __builtin_bit_cast(uint16_t, (_Float16)a);   // RNE
-      if (e & 1) outw[e >> 1] |= (uint32_t)h << 16; else outw[e >> 1] = h;
+      for (int u = 0; u < kCodeBatch; ++u) {
+        const int i = i0 + u * kRowThreads + tid;
+        v[u] = i < 6 * G ? src[i] : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < kCodeBatch; ++u) {
+        const int i = i0 + u * kRowThreads + tid;
+        if (i < 6 * G) grp_s[8 * (i / 6) + i % 6] = v[u];
+      }
     }
-    uint4 v;
-    v.x = outw[0]; v.y = outw[1]; v.z = outw[2]; v.w = outw[3];
-    reinterpret_cast<uint4*>(w)[id] = v;
+#pragma unroll
+    for (int u = 0; u < kGroupBatch; ++u) {
+      const int g = tid + u * kRowThreads;
+      if (g < G) {
+        grp_s[8 * g + 6] = tl[u];
+        grp_s[8 * g + 7] = 0u;
+        scale_s[g] = (uint16_t)sc[u];
+        rec_s[g] = -1;
+      }
+    }
+    if (R > 0) {
+      // The row's records: 6 R code words from 24 k0, then per record its tail
+      // bytes, group index, mu and s1.
+      const uint32_t* rsrc = reinterpret_cast<const uint32_t*>(m.codes1 + 24 * (int64_t)k0);
+      const uint16_t* rtail = reinterpret_cast<const uint16_t*>(m.codes1 + (int64_t)kMainBytes * m.nnz1) + k0;
+      for (int i0 = 0; i0 < 6 * R; i0 += kCodeBatch * kRowThreads) {
+        uint32_t v[kCodeBatch];
+#pragma unroll
+        for (int u = 0; u < kCodeBatch; ++u) {
+          const int i = i0 + u * kRowThreads + tid;
+          v[u] = i < 6 * R ? rsrc[i] : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kCodeBatch; ++u) {
+          const int i = i0 + u * kRowThreads + tid;
+          if (i < 6 * R) rcd_s[8 * (i / 6) + i % 6] = v[u];
+        }
+      }
+      uint32_t rt[kGroupBatch], ms[kGroupBatch];
+      int gi[kGroupBatch];
+#pragma unroll
+      for (int u = 0; u < kGroupBatch; ++u) {
+        const int q = tid + u * kRowThreads;
+        const bool in = q < R;
+        rt[u] = in ? rtail[q] : 0u;
+        ms[u] = in ? ((uint32_t)m.offset1[k0 + q] | ((uint32_t)m.scale1[k0 + q] << 16)) : 0u;
+        gi[u] = in ? (int)m.gidx1[k0 + q] : G;
+      }
+#pragma unroll
+      for (int u = 0; u < kGroupBatch; ++u) {
+        const int q = tid + u * kRowThreads;
+        if (q < R) {
+          rcd_s[8 * q + 6] = rt[u];
+          rcd_s[8 * q + 7] = ms[u];
+          if (gi[u] < G) rec_s[gi[u]] = q;
+        }
+      }
+    }
+    __syncthreads();
+    for (int item = tid; item < 16 * G; item += kRowThreads) {
+      const int g = item >> 4;
+      const int p0 = 8 * (item & 15);    // first of the 8 weights
+      const int j0 = p0 / 5, d0 = p0 - 5 * j0;
+      // Code bytes j0..j0+2 (past byte 25 they read 0; those digits are unused).
+      const uint32_t* gw = grp_s + 8 * g + (j0 >> 2);
+      const uint64_t win = (uint64_t)gw[0] | ((uint64_t)gw[1] << 32);
+      const uint32_t bytes = (uint32_t)(win >> (8 * (j0 & 3)));
+      uint32_t D0 = digits[bytes & 0xFFu] | (digits[(bytes >> 8) & 0xFFu] << 10) |
+                    (digits[(bytes >> 16) & 0xFFu] << 20);
+      D0 >>= 2 * d0;   // digit e of the 8 weights at bits 2e, 2e+1
+      const uint32_t s0 = scale_s[g];
+      const int k = rec_s[g];
+      uint32_t o[4];
+      if (k < 0 && (s0 & 0x7FFFu) != 0 && (s0 & 0x7C00u) != 0x7C00u) {
+        // One plane, finite nonzero scale: +0 + s0*t is exactly +0 or +-s0.
+        const uint32_t S = s0 | ((s0 ^ 0x8000u) << 16);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = __builtin_amdgcn_perm(S, S, selector[(D0 >> (4 * i)) & 15u]);
+      } else {
+        // a = +0; a += mu; a += s0*t0; a += s1*t1 in fp32 (each product exact),
+        // rounded once.
+        const float s0f = half_bits_to_float(s0);
+        float mu = 0.0f, s1f = 0.0f;
+        uint32_t D1 = 0;
+        if (k >= 0) {
+          const uint32_t* rw = rcd_s + 8 * k;
+          mu = half_bits_to_float(rw[7] & 0xFFFFu);
+          s1f = half_bits_to_float(rw[7] >> 16);
+          const uint64_t rwin = (uint64_t)rw[j0 >> 2] | ((uint64_t)rw[(j0 >> 2) + 1] << 32);
+          const uint32_t rb = (uint32_t)(rwin >> (8 * (j0 & 3)));
+          // bytes past 25 come from the mu|s1 word here; their digits are unused
+          D1 = digits[rb & 0xFFu] | (digits[(rb >> 8) & 0xFFu] << 10) | (digits[(rb >> 16) & 0xFFu] << 20);
+          D1 >>= 2 * d0;
+        }
+        uint32_t h[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float t0 = (float)((int)((D0 >> (2 * e)) & 3u) - 1);
+          float a = 0.0f;
+          if (k >= 0) a = a + mu;
+          a = a + s0f * t0;
+          if (k >= 0) {
+            const float t1 = (float)((int)((D1 >> (2 * e)) & 3u) - 1);
+            a = a + s1f * t1;
+          }
+          h[e] = float_to_half_bits(a);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = h[2 * i] | (h[2 * i + 1] << 16);
+      }
+      *reinterpret_cast<uint4*>(w + (f0 + g) * kGroup + p0) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+    __syncthreads();
   }
 }
 
 }  // namespace
 
 hipError_t launch_pack(const int8_t* trits, int64_t n, uint8_t* codes, int32_t* d_err, hipStream_t s) {
-  hipLaunchKernelGGL(pack_kernel, dim3((unsigned)grid_for(kGroupBytes * n)), dim3(kThreads), 0, s,
-                     trits, n, codes, d_err);
+  if ((reinterpret_cast<uintptr_t>(trits) & 15) == 0) {
+    const int64_t blocks = clamp_blocks((n + kPartGroups - 1) / kPartGroups, kPartMaxBlocks);
+    hipLaunchKernelGGL(pack_kernel, dim3((unsigned)blocks), dim3(kPartThreads), 0, s, trits, n, codes, d_err);
+  } else {
+    const int64_t blocks = clamp_blocks((kGroupBytes * n + kByteThreads - 1) / kByteThreads, kMaxBlocks);
+    hipLaunchKernelGGL(pack_bytes_kernel, dim3((unsigned)blocks), dim3(kByteThreads), 0, s, trits, n, codes, d_err);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_unpack(const uint8_t* codes, int64_t n, int8_t* trits, int32_t* d_err, hipStream_t s) {
-  hipLaunchKernelGGL(unpack_kernel, dim3((unsigned)grid_for(kGroupBytes * n)), dim3(kThreads), 0, s,
-                     codes, n, trits, d_err);
+  if ((reinterpret_cast<uintptr_t>(trits) & 15) == 0) {
+    const int64_t blocks = clamp_blocks((n + kPartGroups - 1) / kPartGroups, kPartMaxBlocks);
+    hipLaunchKernelGGL(unpack_kernel, dim3((unsigned)blocks), dim3(kPartThreads), 0, s, codes, n, trits, d_err);
+  } else {
+    const int64_t blocks = clamp_blocks((kGroupBytes * n + kByteThreads - 1) / kByteThreads, kMaxBlocks);
+    hipLaunchKernelGGL(unpack_bytes_kernel, dim3((unsigned)blocks), dim3(kByteThreads), 0, s, codes, n, trits,
+                       d_err);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_validate(const uint8_t* codes, int64_t n, int32_t* d_err, hipStream_t s) {
-  hipLaunchKernelGGL(validate_kernel, dim3((unsigned)grid_for(kGroupBytes * n)), dim3(kThreads), 0, s,
-                     codes, n, d_err);
+  const int64_t chunks = (kGroupBytes * n + 7) / 8;
+  const int64_t blocks = clamp_blocks((chunks + kByteThreads - 1) / kByteThreads, kMaxBlocks);
+  hipLaunchKernelGGL(validate_kernel, dim3((unsigned)blocks), dim3(kByteThreads), 0, s, codes, n, d_err);
   return hipGetLastError();
 }
 
 hipError_t launch_unpack_fp16(const MatDev& m, uint16_t* w, hipStream_t s) {
-  const int64_t work = (int64_t)m.n_out * m.n_groups * 16;
-  hipLaunchKernelGGL(unpack_fp16_kernel, dim3((unsigned)grid_for(work)), dim3(kThreads), 0, s, m, w);
+  const int64_t blocks = clamp_blocks(m.n_out, kRowMaxBlocks);
+  const size_t lds = (size_t)m.n_groups * (2 * 8 * 4 + 4 + 2);
+  hipLaunchKernelGGL(unpack_fp16_kernel, dim3((unsigned)blocks), dim3(kRowThreads), lds, s, m, w);
   return hipGetLastError();
 }
 
