@@ -57,3 +57,20 @@ def test_deterministic():
     X = synth.activations(1024, (12, 0, 0, 1), batch=24)
     a, b = run(case, X, True), run(case, X, True)
     assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+@pytest.mark.parametrize("B", [3, 16, 40, 64])
+@pytest.mark.parametrize("n_out,n_in,f2", [
+    (5000, 512, 0.1),      # two row tiles per workgroup, K split in two
+    (13000, 256, 0.1),     # four row tiles per workgroup, ragged last workgroup
+    (40, 16384, 0.1),      # staging too large: the per-group fallback kernel
+    (100, 8192, 1.0),      # every group two-plane: records staged in several batches
+])
+def test_workgroup_layouts(B, n_out, n_in, f2):
+    log(f"smallbatch layout B={B} {n_out}x{n_in} f2={f2}")
+    case = Case(synth.linear(n_out, n_in, f2, (13, n_out, n_in, B)))
+    X = synth.activations(n_in, (13, n_out, n_in, 98), batch=B, outlier_frac=0.01)
+    got = run(case, X, out_f32=(B % 2 == 0))
+    want = case.oracle_gemm(X)
+    r = assert_within_bound(got, want, case.bound(X), f"B={B} {n_out}x{n_in}")
+    log(f"  max err/bound {r:.3g}")
