@@ -32,16 +32,18 @@
 //   segment with one scalar round trip; the leading arguments that select it
 //   are preloaded into SGPRs.
 // * Plane 1.  Each record is handled by two threads (one per half).  A
-//   record half adds s1 * sum(t1 x) + mu * sum(x) over its half-group into a
-//   per-(row, half-group) LDS slot; the slot array starts at zero.  Records
+//   record half computes s1 * sum(t1 x) + mu * sum(x) over its half-group and
+//   stores it in its own LDS slot (records of a workgroup are contiguous in
+//   CSR order, so the slot is the record's index in that range).  Records
 //   are handled after plane 0.  When the host passes each workgroup's record
 //   range, their loads go out with the first batch; otherwise the range
 //   needs the row pointers first (one more memory round trip).
-// * Reduction.  Plane-0 partials stay in registers; each lane adds its
-//   record slot and the row is summed across its lanes with DPP butterflies
-//   (every lane of a row ends with the same bits), plus one LDS step when a
-//   row spans several waves.  No atomics: results are bit-identical run to
-//   run.
+// * Reduction.  After each pass the lanes of a row add their plane-0 values
+//   with DPP (quad permutes, mirrors and row broadcasts folded into the
+//   adds); the last lane of each 64-lane segment writes the segment sum to
+//   LDS.  After one barrier, one thread per row adds the row's segment sums
+//   and then its records' two halves, always in the same order.  No atomics:
+//   results are bit-identical run to run.
 
 #include "tq_internal.h"
 
