@@ -11,8 +11,9 @@ is far larger than the caches, so every step streams them from HBM.
 Prints one JSON line: value = aggregate GB/s of algorithmic bytes (packed
 weights + activations + outputs) per step time, plus ms_per_step, the
 roofline of the GEMV kernel (its average launch duration: the HIP-event
-timed region on the launch stream over the launches it holds) and the CPU
-oracle timed on a bounded sample.
+timed region on the launch stream over the launches it holds), the measured
+streaming-read ceiling at the same byte count and the CPU oracle timed on a
+bounded sample.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--layers 36]
     python bench.py --extra     # also: small batch, codec, and the 4096 x 2560
@@ -231,6 +232,36 @@ def extra_suite(dev):
     return lines
 
 
+def stream_ceiling(nbytes, dev, reps=5):
+    """Measured streaming-read ceiling at the step's byte count: tq_validate
+    (a 16-byte-per-lane read-reduce kernel) over one buffer of that size,
+    larger than the caches, so each pass streams from HBM."""
+    import torch
+
+    from paper_2609_09240_amd import tq
+    n_groups = nbytes // 26
+    buf = torch.full((26 * n_groups,), 121, dtype=torch.uint8, device=dev)   # valid codes
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        tq.tq_validate(buf, n_groups, d_err=err)
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            a.record(stream)
+            tq.tq_validate(buf, n_groups, d_err=err)
+            b.record(stream)
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b) * 1e-3)
+    assert int(err.item()) == 0
+    t = sorted(times)[len(times) // 2]
+    del buf
+    return {"kernel": "tq_validate read-reduce over one buffer of the step's byte count",
+            "bytes": 26 * n_groups, "us": round(t * 1e6, 2), "GBps": round(26 * n_groups / t / 1e9, 1)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -310,6 +341,9 @@ def main():
     torch.cuda.synchronize()
     del cal, cal_dst
 
+    ceiling = stream_ceiling(step_bytes, dev)
+    log(f"streaming-read ceiling: {ceiling['GBps']:.1f} GB/s")
+
     result = {
         "metric": "packed ternary GEMV HBM GB/s (% of peak) + us per Qwen3-8B decode-step linears",
         "value": round(gbs, 2),
@@ -320,6 +354,8 @@ def main():
         "ms_per_step": round(ms_per_step, 6),
         "us_per_step": round(ms_per_step * 1e3, 2),
         "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+        "pct_of_stream_ceiling": round(100 * gbs / ceiling["GBps"], 2),
+        "stream_ceiling": ceiling,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

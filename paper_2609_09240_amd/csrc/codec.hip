@@ -11,9 +11,11 @@
 // bytes), so every thread moves 8 code bytes and 40-48 trit bytes with vector
 // loads and stores and consecutive lanes touch consecutive memory.  A trit
 // buffer that is not 16-byte aligned takes a one-byte-per-thread kernel.
-// Validate reads the code buffer in flat 8-byte chunks.  The fp16
+// Validate reads the code buffer in flat 16-byte chunks.  The fp16
 // dequantisation stages one row's codes, scales and plane-1 record table in
 // LDS and writes the row with 16-byte stores.
+
+#include <type_traits>
 
 #include "tq_internal.h"
 
@@ -260,52 +262,66 @@ __global__ void __launch_bounds__(kByteThreads) unpack_bytes_kernel(const uint8_
 }
 
 // ---------------------------------------------------------------------------
-// Validate: flat 8-byte chunks.  The main region (24 n bytes) is a multiple
-// of 8, so a chunk is all main bytes or all tail bytes; in the tail, odd
-// bytes are byte 25, whose pad digits 3 and 4 must be 1 (108 <= c <= 134).
+// Validate: flat 16-byte chunks (8-byte chunks when the buffer is only
+// 8-byte aligned).  In the main region (24 n bytes) a byte is bad if it is
+// above 242, counted four bytes at a time; in the tail region odd bytes are
+// byte 25, whose pad digits 3 and 4 must be 1 (108 <= c <= 134).
 // ---------------------------------------------------------------------------
 
+// Bytes above 242 in a word: b >= 243 iff its top bit is set and its low
+// seven bits plus 13 reach 128 (no carry leaves a byte).
 __device__ inline int bad_main(uint32_t w) {
-  int nb = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) nb += ((w >> (8 * i)) & 0xFFu) > 242u;
-  return nb;
+  const uint32_t t = ((w & 0x7F7F7F7Fu) + 0x0D0D0D0Du) & w & 0x80808080u;
+  return __builtin_popcount(t);
 }
 
-__device__ inline int bad_tail(uint32_t w) {
-  int nb = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t c = (w >> (8 * i)) & 0xFFu;
-    nb += (i & 1) ? (c < 108u || c > 134u) : (c > 242u);
-  }
-  return nb;
+// One byte at storage position pos.
+__device__ inline int bad_byte(uint32_t c, int64_t pos, int64_t main_bytes) {
+  if (pos < main_bytes) return c > 242u;
+  return ((pos - main_bytes) & 1) ? (c < 108u || c > 134u) : (c > 242u);
 }
 
+template <int W>   // chunk bytes: 16 or 8
 __global__ void __launch_bounds__(kByteThreads) validate_kernel(const uint8_t* __restrict__ codes, int64_t n,
                                                                 int32_t* d_err) {
+  typedef typename std::conditional<W == 16, uint4, uint2>::type Chunk;
+  constexpr int kWords = W / 4;
   const int64_t total = (int64_t)kGroupBytes * n;
   const int64_t main_bytes = (int64_t)kMainBytes * n;
-  const int64_t chunks = (total + 7) >> 3;
+  const int64_t chunks = (total + W - 1) / W;
   const int64_t stride = (int64_t)gridDim.x * kByteThreads;
   for (int64_t base = (int64_t)blockIdx.x * kByteThreads; base < chunks; base += stride) {
     const int64_t i = base + threadIdx.x;
     int nbad = 0;
     if (i < chunks) {
-      const int64_t pos = 8 * i;
-      uint32_t w0, w1;
-      if (pos + 8 <= total) {
-        const uint2 v = *reinterpret_cast<const uint2*>(codes + pos);
-        w0 = v.x;
-        w1 = v.y;
-      } else {   // last, partial chunk (tail region): missing bytes read as 121, valid everywhere
-        uint32_t b[8];
+      const int64_t pos = (int64_t)W * i;
+      uint32_t w[kWords];
+      if (pos + W <= total) {
+        const Chunk v = *reinterpret_cast<const Chunk*>(codes + pos);
+        w[0] = v.x;
+        w[1] = v.y;
+        if constexpr (W == 16) {
+          w[2] = reinterpret_cast<const uint4&>(v).z;
+          w[3] = reinterpret_cast<const uint4&>(v).w;
+        }
+      } else {   // last, partial chunk: missing bytes read as 121 (valid everywhere)
 #pragma unroll
-        for (int k = 0; k < 8; ++k) b[k] = pos + k < total ? codes[pos + k] : 121u;
-        w0 = b[0] | (b[1] << 8) | (b[2] << 16) | (b[3] << 24);
-        w1 = b[4] | (b[5] << 8) | (b[6] << 16) | (b[7] << 24);
+        for (int k = 0; k < kWords; ++k) {
+          uint32_t x = 0;
+#pragma unroll
+          for (int b = 0; b < 4; ++b) x |= (pos + 4 * k + b < total ? (uint32_t)codes[pos + 4 * k + b] : 121u) << (8 * b);
+          w[k] = x;
+        }
       }
-      nbad = pos < main_bytes ? bad_main(w0) + bad_main(w1) : bad_tail(w0) + bad_tail(w1);
+      if (pos + W <= main_bytes) {
+#pragma unroll
+        for (int k = 0; k < kWords; ++k) nbad += bad_main(w[k]);
+      } else {
+#pragma unroll
+        for (int k = 0; k < kWords; ++k)
+#pragma unroll
+          for (int b = 0; b < 4; ++b) nbad += bad_byte((w[k] >> (8 * b)) & 0xFFu, pos + 4 * k + b, main_bytes);
+      }
     }
     count_errors(d_err, nbad);
   }
@@ -532,9 +548,14 @@ hipError_t launch_unpack(const uint8_t* codes, int64_t n, int8_t* trits, int32_t
 }
 
 hipError_t launch_validate(const uint8_t* codes, int64_t n, int32_t* d_err, hipStream_t s) {
-  const int64_t chunks = (kGroupBytes * n + 7) / 8;
+  const bool wide = (reinterpret_cast<uintptr_t>(codes) & 15) == 0;
+  const int W = wide ? 16 : 8;
+  const int64_t chunks = (kGroupBytes * n + W - 1) / W;
   const int64_t blocks = clamp_blocks((chunks + kByteThreads - 1) / kByteThreads, kMaxBlocks);
-  hipLaunchKernelGGL(validate_kernel, dim3((unsigned)blocks), dim3(kByteThreads), 0, s, codes, n, d_err);
+  if (wide)
+    hipLaunchKernelGGL(validate_kernel<16>, dim3((unsigned)blocks), dim3(kByteThreads), 0, s, codes, n, d_err);
+  else
+    hipLaunchKernelGGL(validate_kernel<8>, dim3((unsigned)blocks), dim3(kByteThreads), 0, s, codes, n, d_err);
   return hipGetLastError();
 }
 
