@@ -14,12 +14,15 @@ What it computes (paper: section 3, eq. 3; section 12):
                    products y = W x and Y = X W^T; the fp32-order dense fp16
                    dequantisation; the per-row acceptance bound.
 * ``accounting`` — the information / storage bit accounting of section 11.
+* ``quantize``   — E2M-ATQ group ternarisation (section 4.2, eqs. 4-6): the
+                   offset, thresholded supports, least-squares scales and
+                   their refinement, and the choice of two-plane groups.
 
-Parity status: codec, packed and accounting are pinned by tests in
+Parity status: codec, packed, accounting and quantize are pinned by tests in
 ``tests/test_oracle_*.py`` (brute force over all codes, exact rational
-arithmetic on tiny shapes, closed-form special cases, and the paper's printed
-bit-accounting figures).  The paper prints no worked packing or GEMV example,
+arithmetic on tiny shapes, closed-form special cases, an independent
+least-squares solver, and the paper's printed bit-accounting figures).  The paper prints no worked packing or GEMV example,
 so agreement with *the paper's own numbers* is pinned only for accounting.
 """
 
-from . import accounting, codec, packed  # noqa: F401
+from . import accounting, codec, packed, quantize  # noqa: F401
