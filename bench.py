@@ -212,6 +212,32 @@ def extra_suite(dev):
                   "GBps": round(nb / us / 1e3, 1)})
     del mats, ws
 
+    # E2M-ATQ ternarisation of a gate-sized fp16 W (12288 x 4096): the
+    # one-plane ranking pass, then the pass with 10% two-plane groups.
+    import numpy as np
+    N, K = 12288, 4096
+    W = torch.randn(N, K, device=dev, dtype=torch.float32).mul_(0.02).to(torch.float16)
+    groups = W.reshape(-1, 128)
+    ng = groups.shape[0]
+    t0b = torch.empty((ng, 128), dtype=torch.int8, device=dev)
+    s0b = torch.empty(ng, dtype=torch.float16, device=dev)
+    eb = torch.empty(ng, dtype=torch.float64, device=dev)
+    t_rank = graph_time_us([lambda: tq.tq_ternarize(groups, iters=0, t0=t0b, s0=s0b, energy=eb)] * 4)
+    sel = tq.select_two_plane(eb.cpu().numpy(), 0.1)
+    nnz = int(sel.size)
+    rec = np.full(ng, -1, dtype=np.int32)
+    rec[sel] = np.arange(nnz, dtype=np.int32)
+    rec_d = torch.from_numpy(rec).to(dev)
+    t1b = torch.empty((nnz, 128), dtype=torch.int8, device=dev)
+    mub = torch.empty(nnz, dtype=torch.float16, device=dev)
+    s1b = torch.empty(nnz, dtype=torch.float16, device=dev)
+    t_fit = graph_time_us([lambda: tq.tq_ternarize(groups, rec_index=rec_d, nnz=nnz, iters=4, t0=t0b, s0=s0b,
+                                                   t1=t1b, offset1=mub, scale1=s1b, want_energy=False)] * 4)
+    lines.append({"bench": "tq_ternarize", "matrix": f"{N}x{K} fp16", "groups": ng,
+                  "rank_pass_us": round(t_rank, 2), "fit_pass_us": round(t_fit, 2), "two_plane_groups": nnz,
+                  "iters": 4, "fit_pass_GBps": round(ng * (256 + 130) / t_fit / 1e3, 1)})
+    del W, groups, t0b, s0b, eb, t1b, mub, s1b, rec_d
+
     # The paper's microbenchmark shape (out 4096, in 2560), cold caches.
     inp = synth.linear(4096, 2560, synth.TWO_PLANE, (9, 4096, 2560, 0))
     x = torch.from_numpy(synth.activations(2560, (9, 4096, 2560, 1))).to(dev)

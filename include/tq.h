@@ -175,6 +175,35 @@ tq_status tq_gemv_grouped(const tq_matrix* ms, int32_t n, const uint16_t* x,
 tq_status tq_gemm_smallbatch(const tq_matrix* m, const uint16_t* X, int32_t B,
                              void* Y, int32_t flags, void* stream);
 
+/* E2M-ATQ ternarisation of 128-weight groups: the planes and scales this
+ * format stores, from dense fp16 weights (section 4.2, eqs. 4-6; the
+ * representation of section 3, eq. 3).
+ *   w          fp16 [n_groups][128], row-major groups; 16-byte aligned
+ *   rec_index  int32 [n_groups], or NULL (every group one-plane): -1 for a
+ *              one-plane group, k in [0, nnz) for a two-plane group whose
+ *              second plane is written as record k (values outside that
+ *              range are one-plane).  Records must be distinct: groups
+ *              naming the same record, and records no group names, are left
+ *              with unspecified contents (always in bounds).
+ *   nnz        number of records (rows of t1, offset1, scale1), >= 0
+ *   iters      refinement sweeps of two-plane groups, 0 <= iters <= 1024
+ *   t0         int8 [n_groups][128] (16-byte aligned), s0 fp16 [n_groups]
+ *   t1         int8 [nnz][128] (16-byte aligned), offset1 and scale1 fp16
+ *              [nnz]; may be NULL when nnz == 0
+ *   energy     fp64 [n_groups] or NULL: ||w - s0*T0||^2 of each group's
+ *              one-plane fit, the ranking used to choose two-plane groups
+ * One-plane groups: T0 = +1 / -1 where w exceeds +0.75 mean|w| / is below
+ * its negation, else 0; s0 = <T0, w> / <T0, T0> (0 on an empty support).
+ * Two-plane groups: mu = mean(w); T0, s0 as above on w - mu; T1, s1 the
+ * same way on the residual w - mu - s0*T0; then `iters` sweeps updating mu,
+ * s0 and s1 in turn with T0, T1 fixed.  Arithmetic is fp64 with every sum
+ * in index order; mu, s0, s1 are rounded once to fp16 (nearest even), so
+ * results are bit-exact and unique.  All buffers are device memory. */
+tq_status tq_ternarize(const uint16_t* w, int64_t n_groups, int32_t group,
+                       const int32_t* rec_index, int64_t nnz, int32_t iters,
+                       int8_t* t0, uint16_t* s0, int8_t* t1, uint16_t* offset1,
+                       uint16_t* scale1, double* energy, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,7 +1,7 @@
 // Internal interface between the host entry points (tq_api.hip) and the
-// kernel launchers (codec.hip, gemv.hip, gemm.hip).  Every launcher assumes
-// its arguments were already checked on the host and returns the status of
-// the launch.
+// kernel launchers (codec.hip, gemv.hip, gemm.hip, quantize.hip).  Every
+// launcher assumes its arguments were already checked on the host and
+// returns the status of the launch.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -45,5 +45,9 @@ hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n,
 
 hipError_t launch_gemm_smallbatch(const MatDev& m, const uint16_t* X, int B,
                                   void* Y, bool out_f32, hipStream_t s);
+
+hipError_t launch_ternarize(const uint16_t* w, int64_t n_groups, const int32_t* rec_index, int64_t nnz,
+                            int iters, int8_t* t0, uint16_t* s0, int8_t* t1, uint16_t* offset1,
+                            uint16_t* scale1, double* energy, hipStream_t s);
 
 }  // namespace tq

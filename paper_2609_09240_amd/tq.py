@@ -73,6 +73,7 @@ def lib():
             "tq_gemv": ([mp, vp, vp, i32, vp], ctypes.c_int),
             "tq_gemv_grouped": ([mp, i32, vp, ctypes.POINTER(ctypes.c_void_p), i32, vp], ctypes.c_int),
             "tq_gemm_smallbatch": ([mp, vp, i32, vp, i32, vp], ctypes.c_int),
+            "tq_ternarize": ([vp, i64, i32, vp, i64, i32, vp, vp, vp, vp, vp, vp, vp], ctypes.c_int),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(L, name)
@@ -263,3 +264,76 @@ def tq_gemm_smallbatch(mat, X, Y=None, out_f32=False, stream=None):
     _check(lib().tq_gemm_smallbatch(ctypes.byref(m), _ptr(X), B, _ptr(Y), OUT_FP32 if out_f32 else OUT_FP16,
                                     _stream(stream)), "tq_gemm_smallbatch")
     return Y
+
+
+def tq_ternarize(w, rec_index=None, nnz=0, iters=4, t0=None, s0=None, t1=None, offset1=None, scale1=None,
+                 energy=None, want_energy=True, stream=None):
+    """E2M-ATQ ternarisation of fp16 groups w [n, 128] (see include/tq.h).
+    Returns (t0, s0, t1, offset1, scale1, energy); t1/offset1/scale1 have nnz
+    rows, energy is fp64 [n] (None unless requested)."""
+    _cuda(w, torch.float16, "w")
+    n = w.numel() // GROUP
+    dev = w.device
+    if t0 is None:
+        t0 = torch.empty((n, GROUP), dtype=torch.int8, device=dev)
+    if s0 is None:
+        s0 = torch.empty(n, dtype=torch.float16, device=dev)
+    if nnz > 0:
+        if t1 is None:
+            t1 = torch.empty((nnz, GROUP), dtype=torch.int8, device=dev)
+        if offset1 is None:
+            offset1 = torch.empty(nnz, dtype=torch.float16, device=dev)
+        if scale1 is None:
+            scale1 = torch.empty(nnz, dtype=torch.float16, device=dev)
+    if rec_index is not None:
+        _cuda(rec_index, torch.int32, "rec_index")
+    if want_energy and energy is None:
+        energy = torch.empty(n, dtype=torch.float64, device=dev)
+    _check(lib().tq_ternarize(_ptr(w), n, GROUP, _ptr(rec_index), nnz, iters, _ptr(t0), _ptr(s0), _ptr(t1),
+                              _ptr(offset1), _ptr(scale1), _ptr(energy), _stream(stream)), "tq_ternarize")
+    return t0, s0, t1, offset1, scale1, energy
+
+
+def select_two_plane(energy, f2):
+    """Host rule for the two-plane subset: the floor(f2 * n) groups with the
+    largest one-plane residual energy, ties to the lower flat index; returns
+    their sorted flat indices (numpy int64)."""
+    import numpy as np
+    e = np.asarray(energy, dtype=np.float64)
+    n = e.size
+    k = int(np.floor(f2 * n))
+    order = np.lexsort((np.arange(n), -e))
+    return np.sort(order[:k])
+
+
+def quantize_linear(W, f2=0.1, iters=4, host_rowptr=True, stream=None):
+    """Packed linear from dense fp16 weights W [N, K] on the GPU: one-plane
+    fits rank the groups, the top f2 get two planes, then tq_ternarize and
+    tq_pack produce the stored planes (section 4.2 and section 12)."""
+    import numpy as np
+    _cuda(W, torch.float16, "W")
+    N, K = W.shape
+    if K % GROUP:
+        raise ValueError("K must be a multiple of 128")
+    ng = K // GROUP
+    groups = W.reshape(N * ng, GROUP)
+    _, _, _, _, _, energy = tq_ternarize(groups, iters=0, stream=stream)
+    sel = select_two_plane(energy.cpu().numpy(), f2)
+    nnz = int(sel.size)
+    rec = np.full(N * ng, -1, dtype=np.int32)
+    rec[sel] = np.arange(nnz, dtype=np.int32)
+    rowptr = np.zeros(N + 1, dtype=np.int32)
+    np.add.at(rowptr, sel // ng + 1, 1)
+    rowptr = np.cumsum(rowptr).astype(np.int32)
+    dev = W.device
+    t0, s0, t1, mu, s1, _ = tq_ternarize(groups, rec_index=torch.from_numpy(rec).to(dev), nnz=nnz, iters=iters,
+                                         want_energy=False, stream=stream)
+    codes0 = tq_pack(t0, stream=stream)
+    kw = {}
+    if nnz:
+        kw = dict(rowptr1=torch.from_numpy(rowptr).to(dev),
+                  gidx1=torch.from_numpy((sel % ng).astype(np.uint16).view(np.int16)).to(dev),
+                  codes1=tq_pack(t1, stream=stream), offset1=mu, scale1=s1)
+        if host_rowptr:
+            kw["rowptr1_host"] = torch.from_numpy(rowptr).contiguous()
+    return PackedLinear(N, K, codes0, s0.reshape(N, ng), **kw)

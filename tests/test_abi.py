@@ -32,7 +32,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for want in ["tq_pack", "tq_unpack", "tq_validate", "tq_unpack_fp16", "tq_gemv", "tq_gemv_grouped",
-                 "tq_gemm_smallbatch", "tq_status_string", "tq_abi_version"]:
+                 "tq_gemm_smallbatch", "tq_ternarize", "tq_status_string", "tq_abi_version"]:
         assert want in names
 
 
@@ -148,6 +148,25 @@ def test_grouped_and_batch_reject_bad_arguments():
     assert L.tq_gemm_smallbatch(ctypes.byref(m), v(FAKE + 2), 4, v(FAKE), 0, None) == 3
     w = ctypes.c_void_p(FAKE + 8)
     assert L.tq_unpack_fp16(ctypes.byref(m), w, None) == 3
+
+
+@no_gpu
+def test_ternarize_rejects_bad_arguments():
+    L = tq.lib()
+    v = ctypes.c_void_p
+    F = v(FAKE)
+
+    def call(w=F, n=4, group=128, rec=None, nnz=0, iters=2, t0=F, s0=F, t1=None, mu=None, s1=None, e=None):
+        return L.tq_ternarize(w, n, group, rec, nnz, iters, t0, s0, t1, mu, s1, e, None)
+
+    assert call(group=64) == 4
+    assert call(n=-1) == 2 and call(nnz=-1) == 2 and call(iters=-1) == 2 and call(iters=1025) == 2
+    assert call(n=0, w=None, t0=None, s0=None) == 0                  # empty: no-op
+    assert call(w=None) == 1 and call(t0=None) == 1 and call(s0=None) == 1
+    assert call(nnz=3) == 1                                           # record outputs required
+    assert call(w=v(FAKE + 8)) == 3 and call(t0=v(FAKE + 4)) == 3 and call(s0=v(FAKE + 1)) == 3
+    assert call(rec=v(FAKE + 2)) == 3 and call(e=v(FAKE + 4)) == 3
+    assert call(nnz=3, t1=v(FAKE + 8), mu=F, s1=F) == 3
 
 
 def test_binding_refuses_cpu_tensors():
