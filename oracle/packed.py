@@ -12,8 +12,11 @@ silent:
   CSR order by row, then group).  On such a group every weight is
   mu + s0*t0 + s1*t1 (the offset applies to all 128 positions); elsewhere it
   is s0*t0.
+* Optionally (the paper's own representation, eq. 3, gives every masked
+  block an offset) every group also carries an fp16 offset mu0[r, g]; its
+  weights are then mu0 + s0*t0 (+ mu + s1*t1 on two-plane groups).
 * x is fp16 and converted exactly.  In fp64 every dequantised weight is exact
-  (a sum of three fp16 values needs at most 42 significant bits) and every
+  (a sum of up to four fp16 values needs at most 42 significant bits) and every
   product w*x is exact, so ``gemv`` and ``gemm`` differ from the exact result
   only by the rounding of the final dot-product sums (about K * 2**-53).
 
@@ -33,13 +36,15 @@ def _two_plane_rows(rowptr1):
 
 
 def dequantize(n_out, n_in, codes0, scale0, rowptr1=None, gidx1=None,
-               codes1=None, offset1=None, scale1=None):
+               codes1=None, offset1=None, scale1=None, offset0=None):
     """Dense fp64 W^ [n_out, n_in] (eq. 3, with the readings above)."""
     assert n_in % G == 0
     ng = n_in // G
     t0, _ = codec.unpack(codes0, n_out * ng)
     s0 = np.asarray(scale0, dtype=np.float16).astype(np.float64)
     w = t0.reshape(n_out, ng, G).astype(np.float64) * s0.reshape(n_out, ng, 1)
+    if offset0 is not None:
+        w += np.asarray(offset0, dtype=np.float16).astype(np.float64).reshape(n_out, ng, 1)
     nnz = 0 if gidx1 is None else int(np.asarray(gidx1).size)
     if nnz:
         rows = _two_plane_rows(rowptr1)
@@ -53,30 +58,31 @@ def dequantize(n_out, n_in, codes0, scale0, rowptr1=None, gidx1=None,
 
 
 def gemv(n_out, n_in, codes0, scale0, rowptr1, gidx1, codes1, offset1,
-         scale1, x):
+         scale1, x, offset0=None):
     """y = W^ x in fp64 for one fp16 activation vector x [n_in]."""
     w = dequantize(n_out, n_in, codes0, scale0, rowptr1, gidx1, codes1,
-                   offset1, scale1)
+                   offset1, scale1, offset0)
     xv = np.asarray(x, dtype=np.float16).astype(np.float64).reshape(n_in)
     return w @ xv
 
 
 def gemm(n_out, n_in, codes0, scale0, rowptr1, gidx1, codes1, offset1,
-         scale1, X):
+         scale1, X, offset0=None):
     """Y = X W^T in fp64 for fp16 activations X [B, n_in] -> [B, n_out]."""
     w = dequantize(n_out, n_in, codes0, scale0, rowptr1, gidx1, codes1,
-                   offset1, scale1)
+                   offset1, scale1, offset0)
     xm = np.asarray(X, dtype=np.float16).astype(np.float64).reshape(-1, n_in)
     return xm @ w.T
 
 
 def dequantize_fp16(n_out, n_in, codes0, scale0, rowptr1=None, gidx1=None,
-                    codes1=None, offset1=None, scale1=None):
+                    codes1=None, offset1=None, scale1=None, offset0=None):
     """Dense fp16 W^ with the fixed fp32 evaluation order, rounded once.
 
-    Each weight is evaluated in float32 as  a = +0;  a = a + mu;
-    a = a + s0*t0;  a = a + s1*t1  (the mu and s1 steps only on two-plane
-    groups; every product s*t is exact), then rounded to fp16 to nearest-even.
+    Each weight is evaluated in float32 as  a = +0;  a = a + mu0;
+    a = a + mu;  a = a + s0*t0;  a = a + s1*t1  (the mu0 step only with
+    per-group offsets, the mu and s1 steps only on two-plane groups; every
+    product s*t is exact), then rounded to fp16 to nearest-even.
     """
     assert n_in % G == 0
     ng = n_in // G
@@ -84,6 +90,8 @@ def dequantize_fp16(n_out, n_in, codes0, scale0, rowptr1=None, gidx1=None,
     t0 = t0.reshape(n_out, ng, G).astype(np.float32)
     s0 = np.asarray(scale0, dtype=np.float16).astype(np.float32).reshape(n_out, ng, 1)
     a = np.zeros((n_out, ng, G), dtype=np.float32)
+    if offset0 is not None:
+        a = a + np.asarray(offset0, dtype=np.float16).astype(np.float32).reshape(n_out, ng, 1)
     nnz = 0 if gidx1 is None else int(np.asarray(gidx1).size)
     if nnz:
         rows = _two_plane_rows(rowptr1)
@@ -99,16 +107,18 @@ def dequantize_fp16(n_out, n_in, codes0, scale0, rowptr1=None, gidx1=None,
 
 
 def error_bound(n_out, n_in, scale0, rowptr1, gidx1, offset1, scale1, X,
-                rel=2e-3):
+                rel=2e-3, offset0=None):
     """Acceptance bound per output: rel * sum_g coef[r, g] * ||x_g||_1.
 
-    coef[r, g] = |s0| + |mu| + |s1| on two-plane groups, |s0| elsewhere: the
-    sum of the magnitudes of the group's affine coefficients, so the bound
-    dominates rel * sum_k |w_k x_k|.  Returns [n_out] for a vector x and
-    [B, n_out] for a matrix X.
+    coef[r, g] = |s0| (+ |mu0| with per-group offsets) (+ |mu| + |s1| on
+    two-plane groups): the sum of the magnitudes of the group's affine
+    coefficients, so the bound dominates rel * sum_k |w_k x_k|.  Returns
+    [n_out] for a vector x and [B, n_out] for a matrix X.
     """
     ng = n_in // G
     coef = np.abs(np.asarray(scale0, dtype=np.float16).astype(np.float64)).reshape(n_out, ng)
+    if offset0 is not None:
+        coef = coef + np.abs(np.asarray(offset0, dtype=np.float16).astype(np.float64)).reshape(n_out, ng)
     nnz = 0 if gidx1 is None else int(np.asarray(gidx1).size)
     if nnz:
         rows = _two_plane_rows(rowptr1)

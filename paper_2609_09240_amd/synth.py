@@ -49,7 +49,7 @@ MLP = ("gate", "up", "down")
 STAGES = (("q", "k", "v"), ("o",), ("gate", "up"), ("down",))
 STAGE_OF = {name: s for s, names in enumerate(STAGES) for name in names}
 
-F_T0, F_S0, F_SEL, F_T1, F_MU, F_S1, F_X = range(7)
+F_T0, F_S0, F_SEL, F_T1, F_MU, F_S1, F_X, F_MU0 = range(8)
 _TERNARY = np.array([-1, -1, -1, 0, 0, 0, 0, 1, 1, 1], dtype=np.int8)
 
 
@@ -78,6 +78,7 @@ class LinearInputs:
     t1: np.ndarray        # int8 [nnz1, 128]
     mu1: np.ndarray       # fp16 [nnz1]
     s1: np.ndarray        # fp16 [nnz1]
+    mu0: np.ndarray = None   # fp16 [n_out, n_in/128]: per-group offsets on every group, or None
 
     @property
     def nnz1(self):
@@ -100,8 +101,9 @@ def selection(n_out, n_in, f2, rng):
     return rowptr, (flat % ng).astype(np.uint16)
 
 
-def linear(n_out, n_in, f2, key, t0=None):
-    """Inputs of one packed linear; ``key`` = (seed, config, layer, proj)."""
+def linear(n_out, n_in, f2, key, t0=None, offset0=False):
+    """Inputs of one packed linear; ``key`` = (seed, config, layer, proj).
+    With ``offset0`` every group also gets an offset mu0 ~ U(-0.01, 0.01)."""
     assert n_in % GROUP == 0 and n_out > 0
     ng = n_in // GROUP
     if t0 is None:
@@ -112,7 +114,8 @@ def linear(n_out, n_in, f2, key, t0=None):
     t1 = ternary(generator(*key, F_T1), (nnz, GROUP))
     mu = fp16_uniform(generator(*key, F_MU), -0.01, 0.01, nnz)
     s1 = fp16_uniform(generator(*key, F_S1), 0.01, 0.05, nnz)
-    return LinearInputs(n_out, n_in, t0, s0, rowptr, gidx, t1, mu, s1)
+    mu0 = fp16_uniform(generator(*key, F_MU0), -0.01, 0.01, (n_out, ng)) if offset0 else None
+    return LinearInputs(n_out, n_in, t0, s0, rowptr, gidx, t1, mu, s1, mu0)
 
 
 def activations(n_in, key, batch=None, outlier_frac=0.0):
@@ -133,6 +136,9 @@ def activations(n_in, key, batch=None, outlier_frac=0.0):
 
 SEED = 0
 TWO_PLANE = 0.10
+# The paper's recorded mask coverages (section 3): 0.5% + 3.1% of blocks carry
+# a second plane.
+PAPER_TWO_PLANE = 0.036
 OUTLIERS = 0.01
 
 

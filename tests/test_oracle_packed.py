@@ -31,7 +31,7 @@ def _args(inp):
 
 
 def oracle_gemv(inp, x):
-    return packed.gemv(*_args(inp), x)
+    return packed.gemv(*_args(inp), x, offset0=inp.mu0)
 
 
 def exact_gemv(inp, x):
@@ -47,9 +47,10 @@ def exact_gemv(inp, x):
         acc = Fraction(0)
         for g in range(ng):
             s0 = Fraction(float(inp.s0[r, g]))
+            m0 = Fraction(float(inp.mu0[r, g])) if inp.mu0 is not None else Fraction(0)
             k = rec.get((r, g))
             for i in range(128):
-                w = s0 * int(inp.t0[r, 128 * g + i])
+                w = m0 + s0 * int(inp.t0[r, 128 * g + i])
                 if k is not None:
                     w += Fraction(float(inp.mu1[k])) + Fraction(float(inp.s1[k])) * int(inp.t1[k, i])
                 acc += w * xf[128 * g + i]
@@ -57,8 +58,8 @@ def exact_gemv(inp, x):
     return y
 
 
-def tiny(n_out, n_in, f2, seed):
-    inp = synth.linear(n_out, n_in, f2, (seed, 9, 0, 0))
+def tiny(n_out, n_in, f2, seed, offset0=False):
+    inp = synth.linear(n_out, n_in, f2, (seed, 9, 0, 0), offset0=offset0)
     x = synth.activations(n_in, (seed, 9, 0, 0))
     return inp, x
 
@@ -66,11 +67,12 @@ def tiny(n_out, n_in, f2, seed):
 # ---------------------------------------------------------------- pins
 
 def pin_exact_rationals(gemv_fn):
-    for (n, k, f2, seed) in [(3, 128, 0.0, 1), (4, 256, 0.5, 2), (8, 512, 0.25, 3), (5, 384, 1.0, 4)]:
-        inp, x = tiny(n, k, f2, seed)
+    for (n, k, f2, seed, off) in [(3, 128, 0.0, 1, False), (4, 256, 0.5, 2, False), (8, 512, 0.25, 3, False),
+                                  (5, 384, 1.0, 4, False), (4, 256, 0.0, 12, True), (6, 512, 0.25, 13, True)]:
+        inp, x = tiny(n, k, f2, seed, offset0=off)
         y = gemv_fn(inp, x)
         ex = exact_gemv(inp, x)
-        mag = np.abs(packed.dequantize(*_args(inp)[:9])) @ np.abs(x.astype(np.float64))
+        mag = np.abs(packed.dequantize(*_args(inp)[:9], offset0=inp.mu0)) @ np.abs(x.astype(np.float64))
         for r in range(n):
             if abs(float(ex[r]) - y[r]) > 1e-12 * max(mag[r], 1e-30):
                 return False
@@ -141,8 +143,36 @@ def pin_negation(gemv_fn):
     return np.allclose(gemv_fn(inp, x), -y, rtol=1e-14, atol=1e-15)
 
 
+def pin_group_offsets_only(gemv_fn):
+    """Per-group offsets with T0 = 0 and one plane: y_r = sum_g mu0[r, g] * sum(x_g)."""
+    inp, x = tiny(5, 512, 0.0, 14, offset0=True)
+    inp.t0[:] = 0
+    y = gemv_fn(inp, x)
+    xs = x.astype(np.float64).reshape(-1, 128).sum(axis=1)
+    want = np.array([sum(float(inp.mu0[r, g]) * xs[g] for g in range(4)) for r in range(5)])
+    return np.allclose(y, want, rtol=1e-12, atol=1e-15)
+
+
+def pin_unit_vectors_with_group_offsets(gemv_fn):
+    """x = e_k with per-group offsets: column k is mu0 + s0*t0 (+ the record)."""
+    inp, _ = tiny(4, 256, 0.5, 15, offset0=True)
+    for col in (3, 200):
+        x = np.zeros(256, np.float16)
+        x[col] = 1.0
+        y = gemv_fn(inp, x)
+        g = col // 128
+        for r in range(4):
+            w = float(inp.mu0[r, g]) + float(inp.s0[r, g]) * int(inp.t0[r, col])
+            for k in range(int(inp.rowptr1[r]), int(inp.rowptr1[r + 1])):
+                if int(inp.gidx1[k]) == g:
+                    w += float(inp.mu1[k]) + float(inp.s1[k]) * int(inp.t1[k, col % 128])
+            if y[r] != w:
+                return False
+    return True
+
+
 PINS = [pin_exact_rationals, pin_unit_vectors, pin_all_plus_one, pin_zero_planes,
-        pin_offset_only, pin_negation]
+        pin_offset_only, pin_negation, pin_group_offsets_only, pin_unit_vectors_with_group_offsets]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda p: p.__name__)
@@ -155,7 +185,12 @@ def test_oracle_gemv_pins(pin):
 def _mutant(kind):
     def gemv_fn(inp, x):
         n, k, c0, s0, rp, gi, c1, mu, s1 = _args(inp)
-        if kind == "drop_offset":
+        mu0 = inp.mu0
+        if kind == "drop_group_offsets":
+            mu0 = None
+        elif kind == "group_offsets_shifted" and mu0 is not None:
+            mu0 = np.roll(mu0, 1, axis=1)
+        elif kind == "drop_offset":
             mu = np.zeros_like(mu)
         elif kind == "drop_plane1":
             s1 = np.zeros_like(s1)
@@ -170,18 +205,19 @@ def _mutant(kind):
             g = (d[..., ::-1] * codec.POW3).sum(-1)
             c0 = codec.to_storage(g.astype(np.uint8))
         elif kind == "transpose":
-            w = packed.dequantize(n, k, c0, s0, rp, gi, c1, mu, s1)
+            w = packed.dequantize(n, k, c0, s0, rp, gi, c1, mu, s1, mu0)
             if n == k:
                 return w.T @ x.astype(np.float64)
             return w @ x.astype(np.float64)[::-1]
         elif kind == "scale_per_row":
             s0 = np.repeat(s0[:, :1], s0.shape[1], axis=1)
-        return packed.gemv(n, k, c0, s0, rp, gi, c1, mu, s1, x)
+        return packed.gemv(n, k, c0, s0, rp, gi, c1, mu, s1, x, offset0=mu0)
     return gemv_fn
 
 
 @pytest.mark.parametrize("kind", ["drop_offset", "drop_plane1", "flip_plane1_sign", "shift_group",
-                                  "reverse_digits", "transpose", "scale_per_row"])
+                                  "reverse_digits", "transpose", "scale_per_row", "drop_group_offsets",
+                                  "group_offsets_shifted"])
 def test_pins_catch_planted_mistakes(kind):
     mutant = _mutant(kind)
     assert not all(pin(mutant) for pin in PINS), kind
@@ -241,3 +277,22 @@ def test_error_bound_dominates_weighted_l1():
     b = packed.error_bound(inp.n_out, inp.n_in, inp.s0, inp.rowptr1, inp.gidx1, inp.mu1, inp.s1, x)
     l1 = np.abs(w) @ np.abs(x.astype(np.float64))
     assert np.all(b >= 2e-3 * l1 * (1 - 1e-12))
+
+
+def test_dense_fp16_with_group_offsets():
+    """With per-group offsets, t = 0 positions of one-plane groups are exactly
+    mu0, and every weight is within one fp16 ulp of the exact mu0 + s0*t0
+    (+ the record)."""
+    inp, _ = tiny(6, 512, 0.25, 16, offset0=True)
+    c0, c1 = _pack(inp)
+    args = (inp.n_out, inp.n_in, c0, inp.s0, inp.rowptr1, inp.gidx1, c1, inp.mu1, inp.s1)
+    w16 = packed.dequantize_fp16(*args, offset0=inp.mu0)
+    exact = packed.dequantize(*args, offset0=inp.mu0)
+    ulp = np.spacing(np.abs(w16).astype(np.float16)).astype(np.float64)
+    assert np.all(np.abs(w16.astype(np.float64) - exact) <= ulp)
+    two = np.zeros((6, 4), bool)
+    two[np.repeat(np.arange(6), np.diff(inp.rowptr1)), inp.gidx1.astype(int)] = True
+    for r in range(6):
+        for c in range(512):
+            if not two[r, c // 128] and inp.t0[r, c] == 0:
+                assert w16[r, c] == inp.mu0[r, c // 128]
