@@ -37,8 +37,10 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def build_stack(layers, device):
-    """Generate (host threads) and pack (GPU) every projection of the stack."""
+def build_stack(layers, device, paper_representation=False):
+    """Generate (host threads) and pack (GPU) every projection of the stack.
+    With ``paper_representation``: an offset on every group and the paper's
+    3.6% two-plane groups instead of the benchmark's 10%."""
     from concurrent.futures import ThreadPoolExecutor
 
     import torch
@@ -47,7 +49,11 @@ def build_stack(layers, device):
     names = [n for n, _, _ in synth.PROJECTIONS]
     mats, xs = [], []
     t0 = time.time()
-    gen = lambda layer: [synth.projection(n, layer, cfg=3) for n in names]  # noqa: E731
+    if paper_representation:
+        gen = lambda layer: [synth.projection(n, layer, cfg=3, f2=synth.PAPER_TWO_PLANE, offset0=True)  # noqa: E731
+                             for n in names]
+    else:
+        gen = lambda layer: [synth.projection(n, layer, cfg=3) for n in names]  # noqa: E731
     with ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
         pending = [ex.submit(gen, layer) for layer in range(min(layers, 8))]
         for layer in range(layers):
@@ -72,6 +78,46 @@ def step_launches(mats, xs):
         for s, names in enumerate(synth.STAGES):
             out.append(([mats[layer][n] for n in names], xs[layer][s]))
     return out
+
+
+def time_stack(mats, xs, steps, warmup):
+    """Capture one decode step of the stack in a HIP graph, replay it
+    `warmup` times, then time `steps` replays; returns (ms per step,
+    launches, graph, outputs)."""
+    import torch
+
+    from paper_2609_09240_amd import tq
+    launches = step_launches(mats, xs)
+    dev = xs[0][0].device
+    outs = [[torch.empty(m.n_out, dtype=torch.float16, device=dev) for m in ms] for ms, _ in launches]
+    stream = torch.cuda.Stream()
+
+    def run_step():
+        for (ms, x), ys in zip(launches, outs):
+            if len(ms) == 1:
+                tq.tq_gemv(ms[0], x, y=ys[0], stream=stream)
+            else:
+                tq.tq_gemv_grouped(ms, x, ys=ys, stream=stream)
+
+    with torch.cuda.stream(stream):
+        run_step()                                  # first launches outside capture
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        run_step()
+    torch.cuda.synchronize()
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_stop = torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        t_start.record(stream)
+        for _ in range(steps):
+            graph.replay()
+        t_stop.record(stream)
+    torch.cuda.synchronize()
+    return t_start.elapsed_time(t_stop) / steps, launches, graph, outs
 
 
 def algorithmic_bytes(launches):
@@ -161,6 +207,26 @@ def copies_of(mat, n):
                 kw[k] = v.clone()
         out.append(type(mat)(**kw))
     return out
+
+
+def paper_representation_line(dev, layers=36, steps=10, warmup=3):
+    """The decode step in the paper's own representation: an offset on every
+    group and 3.6% two-plane groups (section 3), same shapes and protocol."""
+    import torch
+    mats, xs = build_stack(layers, dev, paper_representation=True)
+    ms_per_step, launches, graph, outs = time_stack(mats, xs, steps, warmup)
+    step_bytes = algorithmic_bytes(launches)
+    weight_bytes = sum(m.nbytes() for ms, _ in launches for m in ms)
+    n_weights = sum(m.n_out * m.n_in for ms, _ in launches for m in ms)
+    line = {"bench": "decode_step_paper_representation", "layers": layers, "steps": steps,
+            "two_plane_fraction": 0.036, "group_offsets": "every group",
+            "us_per_step": round(ms_per_step * 1e3, 2),
+            "GBps": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 2),
+            "algorithmic_bytes_per_step": step_bytes,
+            "stored_bits_per_weight": round(8 * weight_bytes / n_weights, 4)}
+    del graph, outs, launches, mats, xs
+    torch.cuda.empty_cache()
+    return line
 
 
 def extra_suite(dev):
@@ -312,42 +378,10 @@ def main():
     torch.cuda.set_device(dev)
 
     mats, xs = build_stack(args.layers, dev)
-    launches = step_launches(mats, xs)
+    ms_per_step, launches, graph, outs = time_stack(mats, xs, args.steps, args.warmup)
     step_bytes = algorithmic_bytes(launches)
     weight_bytes = sum(m.nbytes() for ms, _ in launches for m in ms)
     n_weights = sum(m.n_out * m.n_in for ms, _ in launches for m in ms)
-    outs = [[torch.empty(m.n_out, dtype=torch.float16, device=dev) for m in ms] for ms, _ in launches]
-
-    stream = torch.cuda.Stream()
-
-    def run_step():
-        for (ms, x), ys in zip(launches, outs):
-            if len(ms) == 1:
-                tq.tq_gemv(ms[0], x, y=ys[0], stream=stream)
-            else:
-                tq.tq_gemv_grouped(ms, x, ys=ys, stream=stream)
-
-    with torch.cuda.stream(stream):
-        run_step()                                  # first launches outside capture
-    torch.cuda.synchronize()
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph, stream=stream):
-        run_step()
-    torch.cuda.synchronize()
-
-    for _ in range(args.warmup):
-        graph.replay()
-    torch.cuda.synchronize()
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_stop = torch.cuda.Event(enable_timing=True)
-    with torch.cuda.stream(stream):
-        t_start.record(stream)
-        for _ in range(args.steps):
-            graph.replay()
-        t_stop.record(stream)
-    torch.cuda.synchronize()
-    ms_total = t_start.elapsed_time(t_stop)
-    ms_per_step = ms_total / args.steps
     gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
     log(f"{args.steps} steps: {ms_per_step * 1e3:.1f} us/step, {gbs:.1f} GB/s")
 
@@ -417,6 +451,7 @@ def main():
     if args.extra:
         del graph, outs, launches, mats, xs
         torch.cuda.empty_cache()
+        print(json.dumps(paper_representation_line(dev)), flush=True)
         for line in extra_suite(dev):
             print(json.dumps(line), flush=True)
 

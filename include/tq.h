@@ -65,7 +65,7 @@
 extern "C" {
 #endif
 
-#define TQ_ABI_VERSION 2
+#define TQ_ABI_VERSION 3
 #define TQ_GROUP 128
 #define TQ_GROUP_BYTES 26
 #define TQ_MAX_GROUPS_PER_ROW 256    /* K <= 32768 */
@@ -108,6 +108,12 @@ typedef struct tq_matrix {
    * row pointers first.  It must hold the same values as rowptr1; if it does
    * not, results are unspecified, but every access stays in bounds. */
   const int32_t* rowptr1_host;
+  /* Optional (may be NULL; ABI 3): fp16 [N][G] offset mu0 of EVERY group,
+   * the paper's representation (eq. 3 gives every masked block an offset).
+   * Each weight of group (r, g) is then mu0[r][g] + s0*t0, plus
+   * mu + s1*t1 on two-plane groups; the accuracy bound adds |mu0| to the
+   * group's coefficient.  2-byte aligned. */
+  const uint16_t* offset0;
 } tq_matrix;
 
 /* Version of this ABI (TQ_ABI_VERSION). */
@@ -142,18 +148,21 @@ tq_status tq_validate(const uint8_t* codes, int64_t n_groups, int32_t group,
 /* Dense fp16 dequantisation of a packed linear (eq. 3).
  *   w  fp16 [N][K] row-major; 16-byte aligned
  * Each weight is evaluated in fp32 in the fixed order
- *     a = +0;  a += mu;  a += s0*t0;  a += s1*t1
- * (mu and s1 only on two-plane groups; s*t is exact) and rounded once to
- * fp16, nearest-even, so the result is bit-exact and unique. */
+ *     a = +0;  a += mu0;  a += mu;  a += s0*t0;  a += s1*t1
+ * (mu0 only with per-group offsets, mu and s1 only on two-plane groups;
+ * s*t is exact) and rounded once to fp16, nearest-even, so the result is
+ * bit-exact and unique. */
 tq_status tq_unpack_fp16(const tq_matrix* m, uint16_t* w, void* stream);
 
 /* y = W^ x for one fp16 activation vector (the decode-time GEMV).
  *   x  fp16 [K]; 16-byte aligned
  *   y  [N], fp16 (flags = TQ_OUT_FP16) or fp32 (TQ_OUT_FP32); 4-byte aligned
- * Accumulates sign-selected fp16 activations in fp32, applies s0 per group
- * and mu*sum(x_g) + s1*sum(t1*x_g) per two-plane group.  Accuracy:
- * |y - exact| <= 2e-3 * sum_g (|s0| + [two-plane](|mu| + |s1|)) * ||x_g||_1
- * per output.  x and y must not overlap the matrix buffers. */
+ * Accumulates sign-selected fp16 activations in fp32, applies s0 (and
+ * mu0*sum(x_g) with per-group offsets) per group and mu*sum(x_g) +
+ * s1*sum(t1*x_g) per two-plane group.  Accuracy:
+ * |y - exact| <= 2e-3 * sum_g (|s0| + |mu0| + [two-plane](|mu| + |s1|)) *
+ * ||x_g||_1 per output (|mu0| only with per-group offsets).  x and y must
+ * not overlap the matrix buffers. */
 tq_status tq_gemv(const tq_matrix* m, const uint16_t* x, void* y,
                   int32_t flags, void* stream);
 

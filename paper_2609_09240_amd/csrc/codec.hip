@@ -362,12 +362,13 @@ __device__ inline uint32_t pair_selector(int e) {
 
 // One wave per workgroup, so the LDS writes of a row (table reset, record
 // scatter) take effect in program order without barriers between them.
-// Dynamic LDS, 70 bytes per group of the row:
+// Dynamic LDS, 72 bytes per group of the row:
 //   grp_s  [8 G] words: per group bytes 0..23, 24..25, six zero bytes
 //   rcd_s  [8 G] words: the same for the row's plane-1 records (slot q =
 //          record k - rowptr1[r]), with mu | s1 << 16 in the last word
 //   rec_s  [G]   record slot of each group, or -1
 //   scale_s[G]   s0
+//   off_s  [G]   mu0 (per-group offsets; unused without them)
 constexpr int kCodeBatch = 12;   // code words loaded per thread before one wait (6 G <= 768 in one batch)
 constexpr int kGroupBatch = 4;   // G <= 256 tails and scales per thread in one batch
 
@@ -381,6 +382,9 @@ __global__ void __launch_bounds__(kRowThreads) unpack_fp16_kernel(MatDev m, uint
   uint32_t* rcd_s = dyn + 8 * G;
   int32_t* rec_s = reinterpret_cast<int32_t*>(dyn + 16 * G);
   uint16_t* scale_s = reinterpret_cast<uint16_t*>(rec_s + G);
+  uint16_t* off_s = scale_s + G;
+  const bool has_off = m.offset0 != nullptr;
+  const uint16_t* off_src = has_off ? m.offset0 : m.scale0;   // without offsets: a readable stand-in
   const int tid = threadIdx.x;
   for (int c = tid; c < 256; c += kRowThreads) digits[c] = digit_fields(c);
   if (tid < 16) selector[tid] = pair_selector(tid);
@@ -396,12 +400,13 @@ __global__ void __launch_bounds__(kRowThreads) unpack_fp16_kernel(MatDev m, uint
     // Plane-0 bytes of the row: 6 G words from 24 f0, then 2 G tail bytes.
     const uint32_t* src = reinterpret_cast<const uint32_t*>(m.codes0 + 24 * f0);
     const uint16_t* tsrc = reinterpret_cast<const uint16_t*>(m.codes0 + (int64_t)kMainBytes * n) + f0;
-    uint32_t tl[kGroupBatch], sc[kGroupBatch];
+    uint32_t tl[kGroupBatch], sc[kGroupBatch], mo[kGroupBatch];
 #pragma unroll
     for (int u = 0; u < kGroupBatch; ++u) {
       const int g = tid + u * kRowThreads;
       tl[u] = g < G ? tsrc[g] : 0u;
       sc[u] = g < G ? m.scale0[f0 + g] : 0u;
+      mo[u] = g < G ? off_src[f0 + g] : 0u;
     }
     for (int i0 = 0; i0 < 6 * G; i0 += kCodeBatch * kRowThreads) {
       uint32_t v[kCodeBatch];
@@ -423,6 +428,7 @@ __global__ void __launch_bounds__(kRowThreads) unpack_fp16_kernel(MatDev m, uint
         grp_s[8 * g + 6] = tl[u];
         grp_s[8 * g + 7] = 0u;
         scale_s[g] = (uint16_t)sc[u];
+        off_s[g] = (uint16_t)mo[u];
         rec_s[g] = -1;
       }
     }
@@ -479,15 +485,16 @@ __global__ void __launch_bounds__(kRowThreads) unpack_fp16_kernel(MatDev m, uint
       const uint32_t s0 = scale_s[g];
       const int k = rec_s[g];
       uint32_t o[4];
-      if (k < 0 && (s0 & 0x7FFFu) != 0 && (s0 & 0x7C00u) != 0x7C00u) {
+      if (!has_off && k < 0 && (s0 & 0x7FFFu) != 0 && (s0 & 0x7C00u) != 0x7C00u) {
         // One plane, finite nonzero scale: +0 + s0*t is exactly +0 or +-s0.
         const uint32_t S = s0 | ((s0 ^ 0x8000u) << 16);
 #pragma unroll
         for (int i = 0; i < 4; ++i) o[i] = __builtin_amdgcn_perm(S, S, selector[(D0 >> (4 * i)) & 15u]);
       } else {
-        // a = +0; a += mu; a += s0*t0; a += s1*t1 in fp32 (each product exact),
-        // rounded once.
+        // a = +0; a += mu0; a += mu; a += s0*t0; a += s1*t1 in fp32 (each
+        // product exact), rounded once.
         const float s0f = half_bits_to_float(s0);
+        const float mu0 = half_bits_to_float(off_s[g]);
         float mu = 0.0f, s1f = 0.0f;
         uint32_t D1 = 0;
         if (k >= 0) {
@@ -505,6 +512,7 @@ __global__ void __launch_bounds__(kRowThreads) unpack_fp16_kernel(MatDev m, uint
         for (int e = 0; e < 8; ++e) {
           const float t0 = (float)((int)((D0 >> (2 * e)) & 3u) - 1);
           float a = 0.0f;
+          if (has_off) a = a + mu0;
           if (k >= 0) a = a + mu;
           a = a + s0f * t0;
           if (k >= 0) {
@@ -561,7 +569,7 @@ hipError_t launch_validate(const uint8_t* codes, int64_t n, int32_t* d_err, hipS
 
 hipError_t launch_unpack_fp16(const MatDev& m, uint16_t* w, hipStream_t s) {
   const int64_t blocks = clamp_blocks(m.n_out, kRowMaxBlocks);
-  const size_t lds = (size_t)m.n_groups * (2 * 8 * 4 + 4 + 2);
+  const size_t lds = (size_t)m.n_groups * (2 * 8 * 4 + 4 + 2 + 2);
   hipLaunchKernelGGL(unpack_fp16_kernel, dim3((unsigned)blocks), dim3(kRowThreads), lds, s, m, w);
   return hipGetLastError();
 }

@@ -50,7 +50,7 @@ constexpr int kLutBytes = kLutEntries * kLutCopies * 16;
 
 // Dynamic LDS bytes for P staged pairs and R rows.
 __host__ __device__ constexpr int staged_bytes(int P, int R) {
-  return P * (2 * kSlotBytes + 2 + 1) + 4 * (R + 1);
+  return P * (2 * kSlotBytes + 2 + 2 + 1) + 4 * (R + 1);
 }
 
 struct SbArgs {
@@ -98,7 +98,12 @@ __global__ void __launch_bounds__(64 * RT * KS) sb_kernel(SbArgs a) {
   uint32_t* r_s = reinterpret_cast<uint32_t*>(sbase + P * kSlotBytes);       // [P][8] plane 1
   int* rowptr_s = reinterpret_cast<int*>(sbase + 2 * P * kSlotBytes);        // [R + 1]
   uint16_t* s0_s = reinterpret_cast<uint16_t*>(rowptr_s + R + 1);            // [P]
-  uint8_t* hr_s = reinterpret_cast<uint8_t*>(s0_s + P);                      // [P] record present
+  uint16_t* m0_s = s0_s + P;                                                 // [P] per-group offsets
+  uint8_t* hr_s = reinterpret_cast<uint8_t*>(m0_s + P);                      // [P] record present
+  // Per-group offsets are optional; without them the scales stand in as a
+  // readable address and the staged values are unused.
+  const bool has_off = m.offset0 != nullptr;
+  const uint16_t* off_src = has_off ? m.offset0 : m.scale0;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -124,7 +129,7 @@ __global__ void __launch_bounds__(64 * RT * KS) sb_kernel(SbArgs a) {
   const uint64_t* mainp = reinterpret_cast<const uint64_t*>(m.codes0 + 24 * f0);
   const uint16_t* tailp = reinterpret_cast<const uint16_t*>(m.codes0 + 24 * ngroups) + f0;
   uint64_t pc[kPieces];
-  uint32_t tl[kPairsPerThread], sc[kPairsPerThread];
+  uint32_t tl[kPairsPerThread], sc[kPairsPerThread], mo[kPairsPerThread];
 #pragma unroll
   for (int u = 0; u < kPieces; ++u) pc[u] = mainp[min(tid + u * T, 3 * np - 1)];
 #pragma unroll
@@ -132,6 +137,7 @@ __global__ void __launch_bounds__(64 * RT * KS) sb_kernel(SbArgs a) {
     const int i = min(tid + u * T, np - 1);
     tl[u] = tailp[i];
     sc[u] = m.scale0[f0 + i];
+    mo[u] = off_src[f0 + i];
   }
 
   // ---- 2. Selector table (one entry per thread, written to every copy).
@@ -175,6 +181,7 @@ __global__ void __launch_bounds__(64 * RT * KS) sb_kernel(SbArgs a) {
       const int p = g * R + row;
       w_s[8 * p + 6] = tl[u] | 0x79790000u;
       s0_s[p] = (uint16_t)sc[u];
+      m0_s[p] = (uint16_t)mo[u];
     }
   }
   for (int p = tid; p < P; p += T) hr_s[p] = 0;
@@ -283,7 +290,7 @@ __global__ void __launch_bounds__(64 * RT * KS) sb_kernel(SbArgs a) {
   // record flag and the record slot (read whether or not it is used).
   struct Slot {
     uint4 w0, w1, r0, r1;
-    uint32_t s0, hr;
+    uint32_t s0, m0, hr;
   };
   auto read_slot = [&](int g) {
     const int p = g * R + row_l;
@@ -293,6 +300,7 @@ __global__ void __launch_bounds__(64 * RT * KS) sb_kernel(SbArgs a) {
     v.r0 = *reinterpret_cast<const uint4*>(r_s + 8 * p);
     v.r1 = *reinterpret_cast<const uint4*>(r_s + 8 * p + 4);
     v.s0 = s0_s[p];
+    v.m0 = m0_s[p];
     v.hr = hr_s[p];
     return v;
   };
@@ -316,7 +324,14 @@ __global__ void __launch_bounds__(64 * RT * KS) sb_kernel(SbArgs a) {
     uint4 e[kStepsPerGroup];
 #pragma unroll
     for (int s = 0; s < kStepsPerGroup; ++s) e[s] = lut[((sw[s] >> qsh) & 0xFFu) * kLutCopies + copy];
-    const uint32_t lo0 = cur.s0 ^ 0x8000u, hi0 = cur.s0;   // halves {-s0, +0, +s0}
+    // Halves {-s0, +0, +s0}; with per-group offsets {mu0 - s0, mu0, mu0 + s0},
+    // each rounded once from fp32 as in the dense dequantisation.
+    uint32_t lo0 = cur.s0 ^ 0x8000u, hi0 = cur.s0;
+    if (has_off) {
+      const float m0 = 0.0f + h2f(cur.m0), s0 = h2f(cur.s0);
+      lo0 = f2h(m0 - s0) | (f2h(m0) << 16);
+      hi0 = f2h(m0 + s0);
+    }
     uint32_t av[kStepsPerGroup][3];
 #pragma unroll
     for (int s = 0; s < kStepsPerGroup; ++s) {
@@ -508,22 +523,28 @@ __global__ void __launch_bounds__(kThreads) fallback_kernel(MatDev m, const uint
         const uint16_t s0b = m.scale0[f];
         const int k = recs[r];
         const uint4 p = lut[c0];
-        if (k < 0) {
+        const bool off = m.offset0 != nullptr;
+        if (k < 0 && !off) {
           const half2v s2 = {__builtin_bit_cast(_Float16, s0b), __builtin_bit_cast(_Float16, s0b)};
           o0 = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, p.x) * s2);
           o1 = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, p.y) * s2);
           o2 = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, p.z) * s2);
         } else {
-          const int c1 = m.codes1[byte_offset(k, j, m.nnz1)];
-          const float s0 = h2f(s0b), mu = h2f(m.offset1[k]), s1 = h2f(m.scale1[k]);
+          // a = +0; a += mu0; a += mu; a += s0*t0; a += s1*t1 (the terms
+          // that exist), rounded once.
+          const int c1 = k >= 0 ? m.codes1[byte_offset(k, j, m.nnz1)] : 121;
+          const float s0 = h2f(s0b);
+          const float mu0 = off ? h2f(m.offset0[f]) : 0.0f;
+          const float mu = k >= 0 ? h2f(m.offset1[k]) : 0.0f, s1 = k >= 0 ? h2f(m.scale1[k]) : 0.0f;
           int d0 = c0, d1 = c1;
           uint16_t h[5];
 #pragma unroll
           for (int i = 0; i < 5; ++i) {
             float a = 0.0f;
-            a = a + mu;
+            if (off) a = a + mu0;
+            if (k >= 0) a = a + mu;
             a = a + s0 * (float)(d0 % 3 - 1);
-            a = a + s1 * (float)(d1 % 3 - 1);
+            if (k >= 0) a = a + s1 * (float)(d1 % 3 - 1);
             h[i] = __builtin_bit_cast(uint16_t, (_Float16)a);
             d0 /= 3;
             d1 /= 3;

@@ -31,6 +31,9 @@
 //   is an exact vmcnt.  The matrix record is read from the kernel-argument
 //   segment with one scalar round trip; the leading arguments that select it
 //   are preloaded into SGPRs.
+// * Per-group offsets (optional, on every group): a lane sums its own
+//   activations once and adds mu0 * sum(x) to each pass's value; the
+//   offsets are loaded with the scales.
 // * Plane 1.  Each record is handled by two threads (one per half).  A
 //   record half computes s1 * sum(t1 x) + mu * sum(x) over its half-group and
 //   stores it in its own LDS slot (records of a workgroup are contiguous in
@@ -108,6 +111,7 @@ struct GemvMat {
   const uint8_t* codes1;
   const uint16_t* offset1;
   const uint16_t* scale1;
+  const uint16_t* offset0;   // per-group offsets on every group, or NULL
   void* y;
   int32_t n_out;
   int32_t nnz1;       // < 2^31: the host caps code buffers at 2^32 bytes
@@ -209,18 +213,21 @@ __device__ __attribute__((always_inline)) inline void load_xr(uint32_t (&xr)[kXr
 struct Pass {
   uint32_t w[4];   // w[0..2] body, w[3] tail byte
   uint32_t sc;     // scale bits
+  uint32_t mu;     // per-group offset bits (with offsets)
 };
 
 // Byte offsets fit in 32 bits (the host rejects larger code buffers), so
 // every address is a 64-bit base plus a zero-extended 32-bit offset.
+template <bool kOffset0>
 __device__ inline void load_pass(Pass& p, const uint8_t* body0, const uint8_t* tail0, const uint16_t* scale0,
-                                 uint32_t f) {
+                                 const uint16_t* offset0, uint32_t f) {
   const uint32_t* b = reinterpret_cast<const uint32_t*>(body0 + (size_t)(kMainBytes * f));
   p.w[0] = __builtin_nontemporal_load(b);
   p.w[1] = __builtin_nontemporal_load(b + 1);
   p.w[2] = __builtin_nontemporal_load(b + 2);
   p.w[3] = __builtin_nontemporal_load(tail0 + (size_t)(2 * f));
   p.sc = __builtin_nontemporal_load(scale0 + (size_t)f);
+  if constexpr (kOffset0) p.mu = __builtin_nontemporal_load(offset0 + (size_t)f);
 }
 
 // Where a workgroup reads its records from.
@@ -307,7 +314,7 @@ __device__ inline void store_y(void* y, int i, float v, int out_f32) {
 // kPasses: plane-0 passes per lane, all loaded up front.  kXLoads: 16-byte
 // loads of x per thread (ceil(K / 8 / T)).  kHostRanges: the host passes
 // each workgroup's record range.
-template <int kPasses, int kXLoads, bool kHostRanges>
+template <int kPasses, int kXLoads, bool kHostRanges, bool kOffset0>
 __global__ void __launch_bounds__(kMaxThreads) __attribute__((amdgpu_waves_per_eu(4)))
 gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_per_wg, int32_t out_f32,
             int32_t wb1, int32_t wb2, int32_t wb3, int32_t wb4, int32_t wb5, int32_t wb6, int32_t wb7,
@@ -347,7 +354,8 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
     hk1 = args.rec_begin[w + sel + 1];
   }
   asm volatile("" ::"s"(M.codes0), "s"(M.scale0), "s"(M.rowptr1), "s"(M.gidx1), "s"(M.codes1), "s"(M.offset1),
-               "s"(M.scale1), "s"(M.y), "s"(M.n_out), "s"(M.nnz1), "s"(M.wg_begin), "s"(hk0), "s"(hk1));
+               "s"(M.scale1), "s"(M.offset0), "s"(M.y), "s"(M.n_out), "s"(M.nnz1), "s"(M.wg_begin), "s"(hk0),
+               "s"(hk1));
   __builtin_amdgcn_sched_barrier(0);
   void* const yp = M.y;
   const int row_begin = (w - M.wg_begin) * rows_per_wg;
@@ -411,11 +419,15 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   const uint32_t ngroups = (uint32_t)M.n_out * (uint32_t)G;
   const uint8_t* body0 = M.codes0 + kHalfBytes * h;
   const uint8_t* tail0 = M.codes0 + (size_t)(kMainBytes * ngroups) + h;
+  // A matrix without offsets in a launch with offsets reads its scales in
+  // their place (the values are multiplied by zero).
+  const bool has_off = kOffset0 && M.offset0 != nullptr;
+  const uint16_t* off0 = has_off ? M.offset0 : M.scale0;
   Pass buf[kPasses];
 #pragma unroll
   for (int d = 0; d < kPasses; ++d) {
     const int r = min(row_begin + rl + d * ri, row_end - 1);
-    load_pass(buf[d], body0, tail0, M.scale0, (uint32_t)r * (uint32_t)G + (uint32_t)g);
+    load_pass<kOffset0>(buf[d], body0, tail0, M.scale0, off0, (uint32_t)r * (uint32_t)G + (uint32_t)g);
   }
   asm volatile("" ::: "memory");
   __builtin_amdgcn_sched_barrier(0);
@@ -458,6 +470,15 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   // This lane's activations.
   uint32_t xr[kXrRegs];
   load_xr(xr, xsw, g, h);
+  // With offsets: the sum of this lane's activations (its half of the
+  // group), in a fixed order, for the mu0 * sum(x) term of every pass.
+  float xsum = 0.f;
+  if constexpr (kOffset0) {
+    typedef _Float16 h2v __attribute__((ext_vector_type(2)));
+    const h2v ones = {(_Float16)1.0f, (_Float16)1.0f};
+#pragma unroll
+    for (int i = 0; i < kXrRegs; ++i) xsum = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2v, xr[i]), ones, xsum, false);
+  }
 
   // Plane 0, one row per pass: s0 * sum_i t0 x over each half-group, summed
   // over the row's lanes of this wave.
@@ -466,6 +487,7 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   for (int d = 0; d < kPasses; ++d) {
     const int row = rl + d * ri;
     float v = code_dot(lut, slot, buf[d].w, xr) * h2f(buf[d].sc);
+    if constexpr (kOffset0) v = v + (has_off ? h2f(buf[d].mu) : 0.f) * xsum;
     // Pin the value here: otherwise the dot products sink into the guarded
     // store below while their table reads cannot, and the reads' results of
     // every pass stay live at once.
@@ -516,27 +538,27 @@ constexpr int kPassChoices[] = {1, 2, 3, 4, 6, 8};
 constexpr int kNumPass = 6;
 constexpr int kXChoices[] = {1, 2, 4};
 
-template <int PI, int XI, bool HR>
+template <int PI, int XI, bool HR, bool OFF>
 constexpr GemvKernel kernel_at() {
-  return gemv_kernel<kPassChoices[PI], kXChoices[XI], HR>;
+  return gemv_kernel<kPassChoices[PI], kXChoices[XI], HR, OFF>;
 }
 
-template <bool HR>
+template <bool HR, bool OFF>
 GemvKernel select_kernel_hr(int pi, int xi) {
   static const GemvKernel table[kNumPass][3] = {
-      {kernel_at<0, 0, HR>(), kernel_at<0, 1, HR>(), kernel_at<0, 2, HR>()},
-      {kernel_at<1, 0, HR>(), kernel_at<1, 1, HR>(), kernel_at<1, 2, HR>()},
-      {kernel_at<2, 0, HR>(), kernel_at<2, 1, HR>(), kernel_at<2, 2, HR>()},
-      {kernel_at<3, 0, HR>(), kernel_at<3, 1, HR>(), kernel_at<3, 2, HR>()},
-      {kernel_at<4, 0, HR>(), kernel_at<4, 1, HR>(), kernel_at<4, 2, HR>()},
-      {kernel_at<5, 0, HR>(), kernel_at<5, 1, HR>(), kernel_at<5, 2, HR>()},
+      {kernel_at<0, 0, HR, OFF>(), kernel_at<0, 1, HR, OFF>(), kernel_at<0, 2, HR, OFF>()},
+      {kernel_at<1, 0, HR, OFF>(), kernel_at<1, 1, HR, OFF>(), kernel_at<1, 2, HR, OFF>()},
+      {kernel_at<2, 0, HR, OFF>(), kernel_at<2, 1, HR, OFF>(), kernel_at<2, 2, HR, OFF>()},
+      {kernel_at<3, 0, HR, OFF>(), kernel_at<3, 1, HR, OFF>(), kernel_at<3, 2, HR, OFF>()},
+      {kernel_at<4, 0, HR, OFF>(), kernel_at<4, 1, HR, OFF>(), kernel_at<4, 2, HR, OFF>()},
+      {kernel_at<5, 0, HR, OFF>(), kernel_at<5, 1, HR, OFF>(), kernel_at<5, 2, HR, OFF>()},
   };
   return table[pi][xi];
 }
 
 struct DeviceInfo {
   int cus = 0;
-  bool attr_set[2][kNumPass][3] = {};
+  bool attr_set[2][2][kNumPass][3] = {};
 };
 
 DeviceInfo& device_info() {
@@ -621,6 +643,7 @@ hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n, const uint16_t*
     a.codes1 = ms[i].codes1;
     a.offset1 = ms[i].offset1;
     a.scale1 = ms[i].scale1;
+    a.offset0 = ms[i].offset0;
     a.y = ys[i];
     a.n_out = ms[i].n_out;
     a.nnz1 = (int32_t)ms[i].nnz1;
@@ -652,12 +675,19 @@ hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n, const uint16_t*
   }
 
   const int hr = host_ranges ? 1 : 0;
-  const GemvKernel kern = host_ranges ? select_kernel_hr<true>(pi, xi) : select_kernel_hr<false>(pi, xi);
-  if (!di.attr_set[hr][pi][xi]) {
+  bool any_off = false;
+  for (int i = 0; i < n; ++i) any_off = any_off || ms[i].offset0 != nullptr;
+  const int oi = any_off ? 1 : 0;
+  GemvKernel kern;
+  if (host_ranges)
+    kern = any_off ? select_kernel_hr<true, true>(pi, xi) : select_kernel_hr<true, false>(pi, xi);
+  else
+    kern = any_off ? select_kernel_hr<false, true>(pi, xi) : select_kernel_hr<false, false>(pi, xi);
+  if (!di.attr_set[hr][oi][pi][xi]) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - kLutBytes);
     if (e != hipSuccess) return e;
-    di.attr_set[hr][pi][xi] = true;
+    di.attr_set[hr][oi][pi][xi] = true;
   }
   hipLaunchKernelGGL(kern, dim3(wg), dim3(T), lds_bytes(G, rows_per_wg) - kLutBytes, s, x, G, ri, rows_per_wg,
                      out_f32 ? 1 : 0, wb[1], wb[2], wb[3], wb[4], wb[5], wb[6], wb[7], T, A);

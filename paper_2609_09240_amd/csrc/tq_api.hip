@@ -38,7 +38,7 @@ tq_status check_matrix(const tq_matrix* m, MatDev* d) {
   // Kernels address code buffers with 32-bit byte offsets.
   if ((int64_t)TQ_GROUP_BYTES * m->n_out * G > (int64_t)UINT32_MAX) return TQ_ERR_UNSUPPORTED;
   if (m->codes0 == nullptr || m->scale0 == nullptr) return TQ_ERR_NULL;
-  if (misaligned(m->codes0, 8) || misaligned(m->scale0, 2)) return TQ_ERR_ALIGN;
+  if (misaligned(m->codes0, 8) || misaligned(m->scale0, 2) || misaligned(m->offset0, 2)) return TQ_ERR_ALIGN;
   if (m->nnz1 < 0 || m->nnz1 > m->n_out * G) return TQ_ERR_SHAPE;
   if (m->nnz1 > 0) {
     if (m->rowptr1 == nullptr || m->gidx1 == nullptr || m->codes1 == nullptr || m->offset1 == nullptr ||
@@ -57,6 +57,7 @@ tq_status check_matrix(const tq_matrix* m, MatDev* d) {
   d->offset1 = m->nnz1 > 0 ? m->offset1 : nullptr;
   d->scale1 = m->nnz1 > 0 ? m->scale1 : nullptr;
   d->rowptr1_host = m->nnz1 > 0 ? m->rowptr1_host : nullptr;
+  d->offset0 = m->offset0;
   d->n_out = (int32_t)m->n_out;
   d->n_groups = (int32_t)G;
   return TQ_OK;

@@ -26,6 +26,7 @@ struct MatDev {
   const uint16_t* offset1;
   const uint16_t* scale1;
   const int32_t* rowptr1_host;   // host memory, may be NULL
+  const uint16_t* offset0;       // per-group offsets on every group, may be NULL
   int64_t nnz1;
   int32_t n_out;
   int32_t n_groups;   // groups per row, K / 128

@@ -148,11 +148,12 @@ def single_linear(seed=SEED):
     return linear(1024, 4096, 0.0, key), activations(4096, key)
 
 
-def projection(name, layer=0, cfg=3, seed=SEED, f2=TWO_PLANE):
-    """Packed-linear inputs of one Qwen3-8B projection of ``layer``."""
+def projection(name, layer=0, cfg=3, seed=SEED, f2=TWO_PLANE, offset0=False):
+    """Packed-linear inputs of one Qwen3-8B projection of ``layer`` (with
+    ``offset0``, an offset on every group)."""
     p = PROJ_INDEX[name]
     _, n_out, n_in = PROJECTIONS[p]
-    return linear(n_out, n_in, f2, (seed, cfg, layer, p))
+    return linear(n_out, n_in, f2, (seed, cfg, layer, p), offset0=offset0)
 
 
 def stage_activations(stage, layer=0, cfg=3, seed=SEED, batch=None):

@@ -48,6 +48,7 @@ class TqMatrix(ctypes.Structure):
         ("offset1", ctypes.c_void_p),
         ("scale1", ctypes.c_void_p),
         ("rowptr1_host", ctypes.c_void_p),
+        ("offset0", ctypes.c_void_p),
     ]
 
 
@@ -119,6 +120,7 @@ class PackedLinear:
     offset1: torch.Tensor = None  # float16 [nnz1]
     scale1: torch.Tensor = None   # float16 [nnz1]
     rowptr1_host: torch.Tensor = None  # optional host copy of rowptr1 (int32, CPU)
+    offset0: torch.Tensor = None  # optional float16 [N, G]: an offset on every group
 
     @property
     def nnz1(self):
@@ -142,12 +144,16 @@ class PackedLinear:
             m.scale1 = self.scale1.data_ptr()
             if self.rowptr1_host is not None:
                 m.rowptr1_host = self.rowptr1_host.data_ptr()
+        if self.offset0 is not None:
+            m.offset0 = self.offset0.data_ptr()
         return m
 
     def nbytes(self):
         """Bytes of the packed weights (codes, scales, plane-1 records, CSR)."""
         ng = self.n_groups
         b = GROUP_BYTES * ng + 2 * ng
+        if self.offset0 is not None:
+            b += 2 * ng
         if self.nnz1:
             b += 4 * (self.n_out + 1) + 32 * self.nnz1
         return b
@@ -173,6 +179,8 @@ class PackedLinear:
             )
             if host_rowptr:
                 kw["rowptr1_host"] = torch.from_numpy(inp.rowptr1.astype("int32")).contiguous()
+        if getattr(inp, "mu0", None) is not None:
+            kw["offset0"] = torch.from_numpy(inp.mu0).to(dev)
         return cls(inp.n_out, inp.n_in, codes0, torch.from_numpy(inp.s0).to(dev), **kw)
 
 

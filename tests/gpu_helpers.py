@@ -39,11 +39,14 @@ class Case:
             np.testing.assert_array_equal(self.gpu.codes1.cpu().numpy(), self.c1)
 
     def oracle_gemm(self, X):
-        return packed.gemm(*self.oracle_args(), X)
+        return packed.gemm(*self.oracle_args(), X, offset0=self.inp.mu0)
+
+    def oracle_gemv(self, x):
+        return packed.gemv(*self.oracle_args(), x, offset0=self.inp.mu0)
 
     def bound(self, X):
         i = self.inp
-        return packed.error_bound(i.n_out, i.n_in, i.s0, i.rowptr1, i.gidx1, i.mu1, i.s1, X)
+        return packed.error_bound(i.n_out, i.n_in, i.s0, i.rowptr1, i.gidx1, i.mu1, i.s1, X, offset0=i.mu0)
 
 
 def assert_within_bound(got, want, bound, what):

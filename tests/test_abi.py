@@ -43,7 +43,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert tq.tq_abi_version() == 2
+    assert tq.tq_abi_version() == 3
     for s in range(6):
         assert tq.tq_status_string(s).startswith(tq.STATUS[s])
     assert "unknown" in tq.tq_status_string(42)

@@ -187,3 +187,15 @@ def test_unpack_fp16_special_scales():
     nan_w, nan_g = np.isnan(want), np.isnan(got)
     assert np.array_equal(nan_w, nan_g)
     assert np.array_equal(got.view(np.uint16)[~nan_g], want.view(np.uint16)[~nan_w])
+
+
+@pytest.mark.parametrize("shape,f2", [((64, 256), 0.0), ((96, 512), 0.25), ((1024, 4096), 0.036),
+                                      ((5, 12288), 1.0)])
+def test_unpack_fp16_with_group_offsets(shape, f2):
+    n_out, n_in = shape
+    inp = synth.linear(n_out, n_in, f2, (7, 8, 9, n_out), offset0=True)
+    case = Case(inp)
+    want = packed.dequantize_fp16(*case.oracle_args(), offset0=inp.mu0)
+    got = tq.tq_unpack_fp16(case.gpu)
+    torch.cuda.synchronize()
+    assert np.array_equal(got.cpu().numpy().view(np.uint16), want.view(np.uint16))

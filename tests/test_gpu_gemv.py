@@ -138,3 +138,37 @@ def test_decode_step_layers_sampled(layer):
         for n, c, y in zip(names, cases, ys):
             r = assert_within_bound(y.cpu().numpy(), c.oracle_gemm(x[None])[0], c.bound(x), f"L{layer} {n}")
             log(f"layer {layer} {n}: max err/bound {r:.3g}")
+
+
+# ------------------------------------------------ per-group offsets (ABI 3)
+
+@pytest.mark.parametrize("n_out,n_in,f2", [
+    (1024, 4096, 0.0), (4096, 4096, synth.PAPER_TWO_PLANE), (12288, 4096, synth.PAPER_TWO_PLANE),
+    (4096, 12288, 0.1), (3000, 640, 0.1), (65, 384, 0.5), (1, 128, 1.0), (100, 32768, 0.05),
+])
+def test_group_offsets(n_out, n_in, f2):
+    """An offset on every group (the paper's representation): mu0 * sum(x_g)
+    joins every group, within the bound with |mu0| in each coefficient."""
+    inp = synth.linear(n_out, n_in, f2, (17, n_out, n_in, 0), offset0=True)
+    x = synth.activations(n_in, (17, n_out, n_in, 1), outlier_frac=0.01)
+    case = Case(inp)
+    assert case.gpu.offset0 is not None
+    check(case, x, f"offsets {n_out}x{n_in} f2={f2}", out_f32=True)
+    device_only = Case(inp, host_rowptr=False)
+    assert np.array_equal(run_gemv(device_only, x, True).view(np.uint32), run_gemv(case, x, True).view(np.uint32))
+
+
+def test_grouped_mixes_matrices_with_and_without_offsets():
+    """One launch serves matrices with and without offsets; each output is
+    bit for bit what its own launch gives."""
+    x = synth.activations(4096, (18, 0, 0, 1))
+    cases = [Case(synth.linear(4096, 4096, 0.1, (18, 1, 0, 0), offset0=True)),
+             Case(synth.linear(1024, 4096, 0.1, (18, 2, 0, 0))),
+             Case(synth.linear(1024, 4096, synth.PAPER_TWO_PLANE, (18, 3, 0, 0), offset0=True))]
+    xd = torch.from_numpy(x).cuda()
+    ys = tq.tq_gemv_grouped([c.gpu for c in cases], xd, out_f32=True)
+    singles = [tq.tq_gemv(c.gpu, xd, out_f32=True) for c in cases]
+    torch.cuda.synchronize()
+    for c, yg, y1 in zip(cases, ys, singles):
+        assert torch.equal(yg.view(torch.int32), y1.view(torch.int32))
+        assert_within_bound(yg.cpu().numpy(), c.oracle_gemm(x[None])[0], c.bound(x), "grouped offsets")

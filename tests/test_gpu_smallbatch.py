@@ -74,3 +74,18 @@ def test_workgroup_layouts(B, n_out, n_in, f2):
     want = case.oracle_gemm(X)
     r = assert_within_bound(got, want, case.bound(X), f"B={B} {n_out}x{n_in}")
     log(f"  max err/bound {r:.3g}")
+
+
+@pytest.mark.parametrize("B", [4, 16, 64])
+@pytest.mark.parametrize("n_out,n_in,f2", [
+    (12288, 4096, 0.036), (4096, 12288, 0.1), (5000, 512, 0.1), (40, 16384, 0.1), (100, 1024, 1.0),
+])
+def test_group_offsets(B, n_out, n_in, f2):
+    """Per-group offsets on every group, through every workgroup layout and
+    the fallback kernel."""
+    log(f"smallbatch offsets B={B} {n_out}x{n_in} f2={f2}")
+    case = Case(synth.linear(n_out, n_in, f2, (19, n_out, n_in, B), offset0=True))
+    X = synth.activations(n_in, (19, n_out, n_in, 97), batch=B, outlier_frac=0.01)
+    got = run(case, X, out_f32=True)
+    r = assert_within_bound(got, case.oracle_gemm(X), case.bound(X), f"offsets B={B} {n_out}x{n_in}")
+    log(f"  max err/bound {r:.3g}")
