@@ -22,6 +22,13 @@ Readings where the paper is silent (the packed format fixes the first two):
       s1 <- <T1, w - mu - s0*T0> / <T1, T1>
   (a scale whose support is empty is 0).  The sweeps converge to the joint
   least-squares fit of (mu, s0, s1) for the fixed supports.
+* With an offset on every group (the paper's own representation): a
+  one-plane group is fitted like the first plane of a two-plane group,
+  mu = mean(w), T0 and s0 on w - mu, then ``iters`` sweeps
+      mu <- mean(w - s0*T0);   s0 <- <T0, w - mu> / <T0, T0>;
+  a two-plane group is fitted as above and its mu becomes the group offset
+  (the record's own offset is then 0).  Groups are ranked by the residual
+  energy ||w - mu - s0*T0||^2 of this one-plane fit.
 * The least-squares scale of a support T for a target v is <T, v> / <T, T>,
   i.e. the mean of |v| over the support.
 * Which groups get two planes (the paper's salience masks need calibration
@@ -94,6 +101,28 @@ def fit_two_plane(w, iters):
     return t0, t1, mu, s0, s1
 
 
+def fit_one_plane_offset(w, iters):
+    """One plane with an offset (eqs. 4-6, then the refinement with T0
+    fixed).  Returns (t0, mu, s0) in fp64."""
+    w = np.asarray(w, dtype=np.float64)
+    mu = _sum(w) / w.shape[-1]
+    wc = w - mu[..., None]
+    t0 = threshold_support(wc)
+    s0 = ls_scale(t0, wc)
+    f0 = t0.astype(np.float64)
+    for _ in range(iters):
+        mu = _sum(w - s0[..., None] * f0) / w.shape[-1]
+        s0 = ls_scale(t0, w - mu[..., None])
+    return t0, mu, s0
+
+
+def residual_energy_offset(w, t0, mu, s0):
+    """||w - mu - s0*T0||^2 per group (fp64, index order)."""
+    w = np.asarray(w, dtype=np.float64)
+    d = (w - mu[..., None]) - s0[..., None] * t0.astype(np.float64)
+    return _sum(d * d)
+
+
 def residual_energy(w, t0, s0):
     """||w - s0*T0||^2 per group (fp64, index order): the salience used to
     choose two-plane groups."""
@@ -137,22 +166,54 @@ def ternarize(w, two_plane, iters):
     return t0, t1, to_fp16(s0), to_fp16(mu), to_fp16(s1)
 
 
-def quantize_linear(W, f2, iters):
+def ternarize_with_offsets(w, two_plane, iters):
+    """Per-group result with an offset on every group: (t0, t1, s0, mu0,
+    s1) with mu0 per group, t1 and s1 zero on one-plane groups; scales and
+    offsets rounded to fp16."""
+    w = np.asarray(w, dtype=np.float64)
+    two = np.asarray(two_plane, dtype=bool)
+    n = w.shape[0]
+    t0 = np.zeros((n, G), np.int8)
+    t1 = np.zeros((n, G), np.int8)
+    s0 = np.zeros(n, np.float64)
+    mu0 = np.zeros(n, np.float64)
+    s1 = np.zeros(n, np.float64)
+    one = ~two
+    if one.any():
+        t0[one], mu0[one], s0[one] = fit_one_plane_offset(w[one], iters)
+    if two.any():
+        a, b, c, d, e = fit_two_plane(w[two], iters)
+        t0[two], t1[two], mu0[two], s0[two], s1[two] = a, b, c, d, e
+    return t0, t1, to_fp16(s0), to_fp16(mu0), to_fp16(s1)
+
+
+def quantize_linear(W, f2, iters, group_offsets=False):
     """A packed linear's unpacked inputs from a dense fp16 W [N, K]:
     returns (t0 [N*G', 128], s0 [N, G'], rowptr1, gidx1, t1 [nnz, 128],
-    mu1 [nnz], s1 [nnz]) with G' = K / 128, records in CSR order."""
+    mu1 [nnz], s1 [nnz]) with G' = K / 128, records in CSR order, and with
+    ``group_offsets`` also mu0 [N, G'] (the records' mu1 are then 0)."""
     W = np.asarray(W, dtype=np.float16)
     N, K = W.shape
     assert K % G == 0
     ng = K // G
     groups = W.astype(np.float64).reshape(N * ng, G)
-    t0_1, s0_1 = fit_one_plane(groups)
-    sel = select_two_plane(residual_energy(groups, t0_1, s0_1), f2)
+    if group_offsets:
+        t0_1, mu_1, s0_1 = fit_one_plane_offset(groups, iters)
+        energy = residual_energy_offset(groups, t0_1, mu_1, s0_1)
+    else:
+        t0_1, s0_1 = fit_one_plane(groups)
+        energy = residual_energy(groups, t0_1, s0_1)
+    sel = select_two_plane(energy, f2)
     flags = np.zeros(N * ng, dtype=bool)
     flags[sel] = True
-    t0, t1, s0, mu, s1 = ternarize(groups, flags, iters)
     rows, gidx = sel // ng, sel % ng
     rowptr1 = np.zeros(N + 1, dtype=np.int32)
     np.add.at(rowptr1, rows + 1, 1)
     rowptr1 = np.cumsum(rowptr1).astype(np.int32)
+    if group_offsets:
+        t0, t1, s0, mu0, s1 = ternarize_with_offsets(groups, flags, iters)
+        mu1 = np.zeros(sel.size, np.float16)
+        return (t0, s0.reshape(N, ng), rowptr1, gidx.astype(np.uint16), t1[sel], mu1, s1[sel],
+                mu0.reshape(N, ng))
+    t0, t1, s0, mu, s1 = ternarize(groups, flags, iters)
     return (t0, s0.reshape(N, ng), rowptr1, gidx.astype(np.uint16), t1[sel], mu[sel], s1[sel])

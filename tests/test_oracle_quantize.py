@@ -158,6 +158,39 @@ def quantize_linear_error(W, f2):
     return np.linalg.norm(What - W.astype(np.float64)) / np.linalg.norm(W.astype(np.float64))
 
 
+def test_offset_block_is_recovered_by_the_one_plane_offset_fit():
+    # w = m + c*t with t balanced (mean 0): centring leaves c*t, so T0 = t,
+    # s0 = c and mu = m, a fixed point of the refinement.
+    t = np.tile(np.array([1, -1, 0, 1, -1, 0, 0, 0], np.int8), 16)[None, :]
+    w = 0.25 + 0.0625 * t.astype(np.float64)
+    for iters in (0, 3):
+        t0, mu, s0 = quantize.fit_one_plane_offset(w, iters)
+        assert np.array_equal(t0, t) and mu[0] == 0.25 and s0[0] == 0.0625
+
+
+def test_one_plane_offset_refinement_converges_to_least_squares():
+    r = rng(7)
+    w = fp16_groups(r, 25) + 0.01
+    t0, mu, s0 = quantize.fit_one_plane_offset(w, iters=300)
+    for i in range(25):
+        A = np.stack([np.ones(128), t0[i].astype(float)], axis=1)
+        sol, *_ = np.linalg.lstsq(A, w[i], rcond=None)
+        assert np.allclose([mu[i], s0[i]], sol, rtol=1e-9, atol=1e-12)
+
+
+def test_quantize_linear_with_group_offsets():
+    r = rng(8)
+    N, K = 16, 512
+    W = (r.standard_normal((N, K)) * 0.02 + 0.005).astype(np.float16)
+    t0, s0, rowptr1, gidx1, t1, mu1, s1, mu0 = quantize.quantize_linear(W, 0.036, 3, group_offsets=True)
+    assert np.all(mu1 == 0) and mu0.shape == (N, K // 128)
+    c0 = codec.pack(t0)[0]
+    c1 = codec.pack(t1)[0] if t1.shape[0] else np.zeros(0, np.uint8)
+    What = packed.dequantize(N, K, c0, s0, rowptr1, gidx1, c1, mu1, s1, offset0=mu0)
+    rel_off = np.linalg.norm(What - W.astype(np.float64)) / np.linalg.norm(W.astype(np.float64))
+    assert rel_off < quantize_linear_error(W, 0.036)     # the offsets help on an offset matrix
+
+
 # --------------------------------------------------- planted mistakes (oracle copies)
 
 PINS = [
@@ -171,6 +204,8 @@ PINS = [
     test_refinement_never_increases_the_error,
     test_second_plane_reduces_the_error,
     test_selection_takes_the_largest_energies_with_index_ties,
+    test_offset_block_is_recovered_by_the_one_plane_offset_fit,
+    test_one_plane_offset_refinement_converges_to_least_squares,
 ]
 
 
