@@ -299,10 +299,19 @@ def extra_suite(dev):
     s1b = torch.empty(nnz, dtype=torch.float16, device=dev)
     t_fit = graph_time_us([lambda: tq.tq_ternarize(groups, rec_index=rec_d, nnz=nnz, iters=4, t0=t0b, s0=s0b,
                                                    t1=t1b, offset1=mub, scale1=s1b, want_energy=False)] * 4)
+    # The same two passes with an offset on every group (one-plane groups
+    # then also refine mu and s0).
+    m0b = torch.empty(ng, dtype=torch.float16, device=dev)
+    t_rank_off = graph_time_us([lambda: tq.tq_ternarize(groups, iters=4, t0=t0b, s0=s0b, energy=eb, offset0=m0b)]
+                               * 4)
+    t_fit_off = graph_time_us([lambda: tq.tq_ternarize(groups, rec_index=rec_d, nnz=nnz, iters=4, t0=t0b, s0=s0b,
+                                                       t1=t1b, offset1=mub, scale1=s1b, want_energy=False,
+                                                       offset0=m0b)] * 4)
     lines.append({"bench": "tq_ternarize", "matrix": f"{N}x{K} fp16", "groups": ng,
                   "rank_pass_us": round(t_rank, 2), "fit_pass_us": round(t_fit, 2), "two_plane_groups": nnz,
-                  "iters": 4, "fit_pass_GBps": round(ng * (256 + 130) / t_fit / 1e3, 1)})
-    del W, groups, t0b, s0b, eb, t1b, mub, s1b, rec_d
+                  "iters": 4, "fit_pass_GBps": round(ng * (256 + 130) / t_fit / 1e3, 1),
+                  "group_offsets": {"rank_pass_us": round(t_rank_off, 2), "fit_pass_us": round(t_fit_off, 2)}})
+    del W, groups, t0b, s0b, eb, t1b, mub, s1b, rec_d, m0b
 
     # The paper's microbenchmark shape (out 4096, in 2560), cold caches.
     inp = synth.linear(4096, 2560, synth.TWO_PLANE, (9, 4096, 2560, 0))

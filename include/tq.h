@@ -65,7 +65,7 @@
 extern "C" {
 #endif
 
-#define TQ_ABI_VERSION 3
+#define TQ_ABI_VERSION 4
 #define TQ_GROUP 128
 #define TQ_GROUP_BYTES 26
 #define TQ_MAX_GROUPS_PER_ROW 256    /* K <= 32768 */
@@ -195,14 +195,23 @@ tq_status tq_gemm_smallbatch(const tq_matrix* m, const uint16_t* X, int32_t B,
  *              naming the same record, and records no group names, are left
  *              with unspecified contents (always in bounds).
  *   nnz        number of records (rows of t1, offset1, scale1), >= 0
- *   iters      refinement sweeps of two-plane groups, 0 <= iters <= 1024
+ *   iters      refinement sweeps of every fit that has an offset (two-plane
+ *              groups; with offset0 also one-plane groups), 0..1024
  *   t0         int8 [n_groups][128] (16-byte aligned), s0 fp16 [n_groups]
  *   t1         int8 [nnz][128] (16-byte aligned), offset1 and scale1 fp16
  *              [nnz]; may be NULL when nnz == 0
- *   energy     fp64 [n_groups] or NULL: ||w - s0*T0||^2 of each group's
- *              one-plane fit, the ranking used to choose two-plane groups
- * One-plane groups: T0 = +1 / -1 where w exceeds +0.75 mean|w| / is below
- * its negation, else 0; s0 = <T0, w> / <T0, T0> (0 on an empty support).
+ *   offset0    fp16 [n_groups] or NULL.  Given, every group gets an offset
+ *              (the paper's representation, tq_matrix.offset0): one-plane
+ *              groups are fitted like the first plane below (mu = mean(w),
+ *              then `iters` sweeps of mu <- mean(w - s0*T0),
+ *              s0 <- <T0, w - mu>/<T0, T0>), two-plane groups store their mu
+ *              here and +0 in offset1.
+ *   energy     fp64 [n_groups] or NULL: ||w - mu - s0*T0||^2 of each
+ *              group's one-plane fit (mu = 0 without offset0), the ranking
+ *              used to choose two-plane groups
+ * One-plane groups without offset0: T0 = +1 / -1 where w exceeds
+ * +0.75 mean|w| / is below its negation, else 0; s0 = <T0, w> / <T0, T0>
+ * (0 on an empty support).
  * Two-plane groups: mu = mean(w); T0, s0 as above on w - mu; T1, s1 the
  * same way on the residual w - mu - s0*T0; then `iters` sweeps updating mu,
  * s0 and s1 in turn with T0, T1 fixed.  Arithmetic is fp64 with every sum
@@ -211,7 +220,8 @@ tq_status tq_gemm_smallbatch(const tq_matrix* m, const uint16_t* X, int32_t B,
 tq_status tq_ternarize(const uint16_t* w, int64_t n_groups, int32_t group,
                        const int32_t* rec_index, int64_t nnz, int32_t iters,
                        int8_t* t0, uint16_t* s0, int8_t* t1, uint16_t* offset1,
-                       uint16_t* scale1, double* energy, void* stream);
+                       uint16_t* scale1, uint16_t* offset0, double* energy,
+                       void* stream);
 
 #ifdef __cplusplus
 }

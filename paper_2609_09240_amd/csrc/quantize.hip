@@ -12,7 +12,11 @@
 //   mu, s0, s1 in turn with the supports fixed (block coordinate descent on
 //   the squared error);
 // * for every group, the residual energy ||w - s0 T0||^2 of the one-plane
-//   fit, which ranks groups for the second plane.
+//   fit, which ranks groups for the second plane;
+// * with an offset on every group (the paper's own representation), the
+//   one-plane fit also takes mu = mean(w), thresholds w - mu and refines mu
+//   and s0; two-plane groups store their mu as the group's offset and 0 as
+//   the record's.
 //
 // Two launches: every group's one-plane fit (and its energy), then the
 // two-plane groups alone, one thread per record.  A thread owns one group
@@ -121,8 +125,9 @@ __device__ inline void load_group(uint16_t* w_s, const uint16_t* __restrict__ w,
 // the two fits).
 __global__ void __launch_bounds__(kThreads) one_plane_kernel(const uint16_t* __restrict__ w, int64_t n,
                                                              const int32_t* __restrict__ rec_index, int64_t nnz,
-                                                             int8_t* __restrict__ t0_out, uint16_t* __restrict__ s0_out,
-                                                             int8_t* __restrict__ t1_out,
+                                                             int iters, int8_t* __restrict__ t0_out,
+                                                             uint16_t* __restrict__ s0_out, int8_t* __restrict__ t1_out,
+                                                             uint16_t* __restrict__ off0_out,
                                                              double* __restrict__ energy_out) {
   __shared__ uint16_t w_s[kGroup * kThreads];
   __shared__ int8_t t0_s[kGroup * kThreads];
@@ -135,22 +140,42 @@ __global__ void __launch_bounds__(kThreads) one_plane_kernel(const uint16_t* __r
     load_group(w_s, w, f, tid);
     int64_t k = rec_index != nullptr ? (int64_t)rec_index[f] : -1;
     if (k >= nnz) k = -1;
+    // Without group offsets mu stays 0 (the raw weights are thresholded);
+    // with them mu starts at the mean and is refined with s0.
+    double mu = 0.0;
+    if (off0_out != nullptr) {
+      double sw = 0.0;
+      for (int i = 0; i < kGroup; ++i) sw = sw + g.wat(i);
+      mu = sw / kGroup;
+    }
+    const double mu_c = mu;
     double sabs = 0.0;
-    for (int i = 0; i < kGroup; ++i) sabs = sabs + fabs(g.wat(i));
+    for (int i = 0; i < kGroup; ++i) sabs = sabs + fabs(g.wat(i) - mu_c);
     const double delta = kThreshold * (sabs / kGroup);
     int n_one = 0;
     double num = 0.0;
     for (int i = 0; i < kGroup; ++i) {
-      const int8_t t = threshold(g.wat(i), delta);
+      const double v = g.wat(i) - mu_c;
+      const int8_t t = threshold(v, delta);
       t0_s[i * kThreads + tid] = t;
       n_one += t != 0;
-      num = num + (double)t * g.wat(i);
+      num = num + (double)t * v;
     }
-    const double s0_one = ls_ratio(num, n_one);
+    double s0_one = ls_ratio(num, n_one);
+    if (off0_out != nullptr) {
+      for (int it = 0; it < iters; ++it) {
+        double a = 0.0;
+        for (int i = 0; i < kGroup; ++i) a = a + (g.wat(i) - s0_one * g.t0at(i));
+        mu = a / kGroup;
+        double b = 0.0;
+        for (int i = 0; i < kGroup; ++i) b = b + g.t0at(i) * (g.wat(i) - mu);
+        s0_one = ls_ratio(b, n_one);
+      }
+    }
     if (energy_out != nullptr) {
       double e = 0.0;
       for (int i = 0; i < kGroup; ++i) {
-        const double d = g.wat(i) - s0_one * g.t0at(i);
+        const double d = (g.wat(i) - mu) - s0_one * g.t0at(i);
         e = e + d * d;
       }
       energy_out[f] = e;
@@ -158,6 +183,7 @@ __global__ void __launch_bounds__(kThreads) one_plane_kernel(const uint16_t* __r
     if (k < 0) {
       store_trits(t0_out + f * kGroup, t0_s, tid);
       s0_out[f] = f64_to_f16(s0_one);
+      if (off0_out != nullptr) off0_out[f] = f64_to_f16(mu);
     } else {
       *reinterpret_cast<int64_t*>(t1_out + k * kGroup) = f;
     }
@@ -170,7 +196,8 @@ __global__ void __launch_bounds__(kThreads) two_plane_kernel(const uint16_t* __r
                                                              const int32_t* __restrict__ rec_index, int64_t nnz,
                                                              int iters, int8_t* __restrict__ t0_out,
                                                              uint16_t* __restrict__ s0_out, int8_t* __restrict__ t1_out,
-                                                             uint16_t* __restrict__ mu_out, uint16_t* __restrict__ s1_out) {
+                                                             uint16_t* __restrict__ mu_out, uint16_t* __restrict__ s1_out,
+                                                             uint16_t* __restrict__ off0_out) {
   __shared__ uint16_t w_s[kGroup * kThreads];
   __shared__ int8_t t0_s[kGroup * kThreads];
   __shared__ int8_t t1_s[kGroup * kThreads];
@@ -229,7 +256,12 @@ __global__ void __launch_bounds__(kThreads) two_plane_kernel(const uint16_t* __r
     store_trits(t0_out + f * kGroup, t0_s, tid);
     s0_out[f] = f64_to_f16(s0);
     store_trits(t1_out + k * kGroup, t1_s, tid);
-    mu_out[k] = f64_to_f16(mu);
+    if (off0_out != nullptr) {   // the offset belongs to the group; the record's is 0
+      off0_out[f] = f64_to_f16(mu);
+      mu_out[k] = 0;
+    } else {
+      mu_out[k] = f64_to_f16(mu);
+    }
     s1_out[k] = f64_to_f16(s1);
   }
 }
@@ -237,19 +269,19 @@ __global__ void __launch_bounds__(kThreads) two_plane_kernel(const uint16_t* __r
 }  // namespace
 
 hipError_t launch_ternarize(const uint16_t* w, int64_t n, const int32_t* rec_index, int64_t nnz, int iters,
-                            int8_t* t0, uint16_t* s0, int8_t* t1, uint16_t* mu, uint16_t* s1, double* energy,
-                            hipStream_t s) {
+                            int8_t* t0, uint16_t* s0, int8_t* t1, uint16_t* mu, uint16_t* s1, uint16_t* off0,
+                            double* energy, hipStream_t s) {
   auto blocks_for = [](int64_t work) {
     const int64_t b = (work + kThreads - 1) / kThreads;
     return (unsigned)(b < 1 ? 1 : (b > kMaxBlocks ? kMaxBlocks : b));
   };
   const bool two = rec_index != nullptr && nnz > 0;
   hipLaunchKernelGGL(one_plane_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s, w, n, two ? rec_index : nullptr,
-                     two ? nnz : 0, t0, s0, t1, energy);
+                     two ? nnz : 0, iters, t0, s0, t1, off0, energy);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !two) return e;
   hipLaunchKernelGGL(two_plane_kernel, dim3(blocks_for(nnz)), dim3(kThreads), 0, s, w, n, rec_index, nnz, iters, t0,
-                     s0, t1, mu, s1);
+                     s0, t1, mu, s1, off0);
   return hipGetLastError();
 }
 

@@ -164,7 +164,7 @@ tq_status tq_gemm_smallbatch(const tq_matrix* m, const uint16_t* X, int32_t B, v
 
 tq_status tq_ternarize(const uint16_t* w, int64_t n_groups, int32_t group, const int32_t* rec_index, int64_t nnz,
                        int32_t iters, int8_t* t0, uint16_t* s0, int8_t* t1, uint16_t* offset1, uint16_t* scale1,
-                       double* energy, void* stream) {
+                       uint16_t* offset0, double* energy, void* stream) {
   if (group != TQ_GROUP) return TQ_ERR_UNSUPPORTED;
   if (n_groups < 0 || nnz < 0 || n_groups > (INT64_MAX / 256) || iters < 0 || iters > 1024) return TQ_ERR_SHAPE;
   if (n_groups == 0) return TQ_OK;
@@ -174,8 +174,9 @@ tq_status tq_ternarize(const uint16_t* w, int64_t n_groups, int32_t group, const
   if (rec_index != nullptr && misaligned(rec_index, 4)) return TQ_ERR_ALIGN;
   if (nnz > 0 && (misaligned(t1, 16) || misaligned(offset1, 2) || misaligned(scale1, 2))) return TQ_ERR_ALIGN;
   if (energy != nullptr && misaligned(energy, 8)) return TQ_ERR_ALIGN;
-  return from_hip(tq::launch_ternarize(w, n_groups, rec_index, nnz, iters, t0, s0, t1, offset1, scale1, energy,
-                                       (hipStream_t)stream));
+  if (offset0 != nullptr && misaligned(offset0, 2)) return TQ_ERR_ALIGN;
+  return from_hip(tq::launch_ternarize(w, n_groups, rec_index, nnz, iters, t0, s0, t1, offset1, scale1, offset0,
+                                       energy, (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -49,6 +49,6 @@ hipError_t launch_gemm_smallbatch(const MatDev& m, const uint16_t* X, int B,
 
 hipError_t launch_ternarize(const uint16_t* w, int64_t n_groups, const int32_t* rec_index, int64_t nnz,
                             int iters, int8_t* t0, uint16_t* s0, int8_t* t1, uint16_t* offset1,
-                            uint16_t* scale1, double* energy, hipStream_t s);
+                            uint16_t* scale1, uint16_t* offset0, double* energy, hipStream_t s);
 
 }  // namespace tq

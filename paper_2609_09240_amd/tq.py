@@ -16,6 +16,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtq.so")
 
+ABI_VERSION = 4
 GROUP = 128
 GROUP_BYTES = 26
 OUT_FP16 = 0
@@ -74,12 +75,15 @@ def lib():
             "tq_gemv": ([mp, vp, vp, i32, vp], ctypes.c_int),
             "tq_gemv_grouped": ([mp, i32, vp, ctypes.POINTER(ctypes.c_void_p), i32, vp], ctypes.c_int),
             "tq_gemm_smallbatch": ([mp, vp, i32, vp, i32, vp], ctypes.c_int),
-            "tq_ternarize": ([vp, i64, i32, vp, i64, i32, vp, vp, vp, vp, vp, vp, vp], ctypes.c_int),
+            "tq_ternarize": ([vp, i64, i32, vp, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp], ctypes.c_int),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(L, name)
             fn.argtypes = args
             fn.restype = res
+        if L.tq_abi_version() != ABI_VERSION:
+            raise RuntimeError(f"{LIB_PATH} implements ABI {L.tq_abi_version()}, the binding expects "
+                               f"{ABI_VERSION}: rebuild it with __graft_entry__.build()")
         _lib = L
     return _lib
 
@@ -275,10 +279,11 @@ def tq_gemm_smallbatch(mat, X, Y=None, out_f32=False, stream=None):
 
 
 def tq_ternarize(w, rec_index=None, nnz=0, iters=4, t0=None, s0=None, t1=None, offset1=None, scale1=None,
-                 energy=None, want_energy=True, stream=None):
+                 energy=None, want_energy=True, offset0=None, group_offsets=False, stream=None):
     """E2M-ATQ ternarisation of fp16 groups w [n, 128] (see include/tq.h).
-    Returns (t0, s0, t1, offset1, scale1, energy); t1/offset1/scale1 have nnz
-    rows, energy is fp64 [n] (None unless requested)."""
+    Returns (t0, s0, t1, offset1, scale1, energy, offset0); t1/offset1/scale1
+    have nnz rows, energy is fp64 [n] (None unless requested), offset0 is
+    fp16 [n] with ``group_offsets`` (or when passed in), else None."""
     _cuda(w, torch.float16, "w")
     n = w.numel() // GROUP
     dev = w.device
@@ -297,9 +302,12 @@ def tq_ternarize(w, rec_index=None, nnz=0, iters=4, t0=None, s0=None, t1=None, o
         _cuda(rec_index, torch.int32, "rec_index")
     if want_energy and energy is None:
         energy = torch.empty(n, dtype=torch.float64, device=dev)
+    if group_offsets and offset0 is None:
+        offset0 = torch.empty(n, dtype=torch.float16, device=dev)
     _check(lib().tq_ternarize(_ptr(w), n, GROUP, _ptr(rec_index), nnz, iters, _ptr(t0), _ptr(s0), _ptr(t1),
-                              _ptr(offset1), _ptr(scale1), _ptr(energy), _stream(stream)), "tq_ternarize")
-    return t0, s0, t1, offset1, scale1, energy
+                              _ptr(offset1), _ptr(scale1), _ptr(offset0), _ptr(energy), _stream(stream)),
+           "tq_ternarize")
+    return t0, s0, t1, offset1, scale1, energy, offset0
 
 
 def select_two_plane(energy, f2):
@@ -314,10 +322,12 @@ def select_two_plane(energy, f2):
     return np.sort(order[:k])
 
 
-def quantize_linear(W, f2=0.1, iters=4, host_rowptr=True, stream=None):
+def quantize_linear(W, f2=0.1, iters=4, host_rowptr=True, group_offsets=False, stream=None):
     """Packed linear from dense fp16 weights W [N, K] on the GPU: one-plane
     fits rank the groups, the top f2 get two planes, then tq_ternarize and
-    tq_pack produce the stored planes (section 4.2 and section 12)."""
+    tq_pack produce the stored planes (section 4.2 and section 12).  With
+    ``group_offsets`` every group carries an offset (offset0), the paper's
+    own representation of section 3, eq. 3."""
     import numpy as np
     _cuda(W, torch.float16, "W")
     N, K = W.shape
@@ -325,7 +335,9 @@ def quantize_linear(W, f2=0.1, iters=4, host_rowptr=True, stream=None):
         raise ValueError("K must be a multiple of 128")
     ng = K // GROUP
     groups = W.reshape(N * ng, GROUP)
-    _, _, _, _, _, energy = tq_ternarize(groups, iters=0, stream=stream)
+    # The ranking fit: with offsets its refinement decides the energy.
+    energy = tq_ternarize(groups, iters=iters if group_offsets else 0, group_offsets=group_offsets,
+                          stream=stream)[5]
     sel = select_two_plane(energy.cpu().numpy(), f2)
     nnz = int(sel.size)
     rec = np.full(N * ng, -1, dtype=np.int32)
@@ -334,8 +346,9 @@ def quantize_linear(W, f2=0.1, iters=4, host_rowptr=True, stream=None):
     np.add.at(rowptr, sel // ng + 1, 1)
     rowptr = np.cumsum(rowptr).astype(np.int32)
     dev = W.device
-    t0, s0, t1, mu, s1, _ = tq_ternarize(groups, rec_index=torch.from_numpy(rec).to(dev), nnz=nnz, iters=iters,
-                                         want_energy=False, stream=stream)
+    t0, s0, t1, mu, s1, _, mu0 = tq_ternarize(groups, rec_index=torch.from_numpy(rec).to(dev), nnz=nnz,
+                                              iters=iters, want_energy=False, group_offsets=group_offsets,
+                                              stream=stream)
     codes0 = tq_pack(t0, stream=stream)
     kw = {}
     if nnz:
@@ -344,4 +357,6 @@ def quantize_linear(W, f2=0.1, iters=4, host_rowptr=True, stream=None):
                   codes1=tq_pack(t1, stream=stream), offset1=mu, scale1=s1)
         if host_rowptr:
             kw["rowptr1_host"] = torch.from_numpy(rowptr).contiguous()
+    if group_offsets:
+        kw["offset0"] = mu0.reshape(N, ng)
     return PackedLinear(N, K, codes0, s0.reshape(N, ng), **kw)

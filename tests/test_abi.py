@@ -43,7 +43,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert tq.tq_abi_version() == 3
+    assert tq.tq_abi_version() == tq.ABI_VERSION == 4
     for s in range(6):
         assert tq.tq_status_string(s).startswith(tq.STATUS[s])
     assert "unknown" in tq.tq_status_string(42)
@@ -156,8 +156,9 @@ def test_ternarize_rejects_bad_arguments():
     v = ctypes.c_void_p
     F = v(FAKE)
 
-    def call(w=F, n=4, group=128, rec=None, nnz=0, iters=2, t0=F, s0=F, t1=None, mu=None, s1=None, e=None):
-        return L.tq_ternarize(w, n, group, rec, nnz, iters, t0, s0, t1, mu, s1, e, None)
+    def call(w=F, n=4, group=128, rec=None, nnz=0, iters=2, t0=F, s0=F, t1=None, mu=None, s1=None, m0=None,
+             e=None):
+        return L.tq_ternarize(w, n, group, rec, nnz, iters, t0, s0, t1, mu, s1, m0, e, None)
 
     assert call(group=64) == 4
     assert call(n=-1) == 2 and call(nnz=-1) == 2 and call(iters=-1) == 2 and call(iters=1025) == 2
@@ -165,7 +166,7 @@ def test_ternarize_rejects_bad_arguments():
     assert call(w=None) == 1 and call(t0=None) == 1 and call(s0=None) == 1
     assert call(nnz=3) == 1                                           # record outputs required
     assert call(w=v(FAKE + 8)) == 3 and call(t0=v(FAKE + 4)) == 3 and call(s0=v(FAKE + 1)) == 3
-    assert call(rec=v(FAKE + 2)) == 3 and call(e=v(FAKE + 4)) == 3
+    assert call(rec=v(FAKE + 2)) == 3 and call(e=v(FAKE + 4)) == 3 and call(m0=v(FAKE + 1)) == 3
     assert call(nnz=3, t1=v(FAKE + 8), mu=F, s1=F) == 3
 
 
