@@ -25,10 +25,16 @@
 //   three times as many LDS cycles in bank conflicts).
 // * Loads.  Per pass a lane loads 12 body bytes (three dwords, 4-aligned in
 //   the split layout), its tail byte and its group's scale; lanes of a row
-//   read consecutive bytes, so every wave load is contiguous.  All loads of a
-//   workgroup are issued before its first wait, in the order their data is
-//   needed, and every one is unconditional (clamped addresses), so each wait
-//   is an exact vmcnt.  The matrix record is read from the kernel-argument
+//   read consecutive bytes, so every wave load is contiguous.  Every wave
+//   issues its x loads before any wave issues weight loads (a barrier
+//   between), then the records' and the first two passes' loads; each later
+//   pass is issued after the pass two before it is computed (issuing every
+//   pass up front stalls the waves at issue, and the set-up with them).
+//   Loads go out in the order their data is needed and every one is
+//   unconditional (clamped addresses), so each wait is an exact vmcnt.
+//   x is staged in LDS with each half-group's 60 inputs 16-byte aligned, so
+//   a lane fetches its activations with ten reads.  The matrix record is read
+//   from the kernel-argument
 //   segment with one scalar round trip; the leading arguments that select it
 //   are preloaded into SGPRs.
 // * Per-group offsets (optional, on every group): a lane sums its own
@@ -62,12 +68,23 @@ constexpr int kLutBytes = 256 * kRep * 16;
 constexpr int kMaxThreads = 1024;
 constexpr int kHalfBytes = 12;                 // body bytes per half-group
 constexpr int kLaneBytes = kHalfBytes + 1;     // + one tail byte
-// x in LDS: group g at dword 65 g (130 halves).  The odd dword stride puts
-// the 64 lanes of a wave (32 groups x 2 halves) on different banks when they
-// read their activations.
-constexpr int kXStrideDw = 65;
+// x in LDS: group g at dword 68 g, inputs 0..59 at dwords 0..29, inputs
+// 60..119 at 32..61, inputs 120..127 at 62..65 (dwords 30, 31, 66, 67
+// unused).  Each half's 30 body dwords then start 16-byte aligned, and the
+// 16 lanes that one 16-byte LDS read serves together (8 groups x 2 halves)
+// cover the 64 banks exactly once.
+constexpr int kXStrideDw = 68;
+constexpr int kXHalfDw = 32;   // dword offset of half 1's body
+constexpr int kXTailDw = 62;   // dword offset of inputs 120..127
+
+// Dword offset within a group's slot of inputs i .. i+3 (i % 4 == 0).
+__device__ inline int x_slot_dw(int i) {
+  return i < 60 ? i / 2 : (i < 120 ? kXHalfDw + (i - 60) / 2 : kXTailDw + (i - 120) / 2);
+}
 // Record-range table entries passed with a launch (host ranges).
 constexpr int kMaxRangeEntries = 768;
+// Plane-0 passes whose loads are issued before the set-up.
+constexpr int kPrefetch = 2;
 
 static_assert(kRep == 16, "the table addressing assumes 16 copies");
 
@@ -187,26 +204,42 @@ __device__ __attribute__((always_inline)) inline float code_dot(const unsigned c
 
 // Activations of half h of group g from the LDS copy of x: 12 body bytes
 // (inputs 60h + 5j ..) and the tail byte (inputs 120 + 5h ..); inputs past
-// the group (pad digits) are zero.
+// the group (pad digits) are zero.  Seven 16-byte reads, one 8-byte read for
+// the body and two for the tail.
 __device__ __attribute__((always_inline)) inline void load_xr(uint32_t (&xr)[kXrRegs], const uint32_t* xsw, int g,
                                                               int h) {
-  const uint32_t* xd = xsw + kXStrideDw * g + 30 * h;   // inputs 60 h ..
+  typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+  typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+  const uint32_t* xg = xsw + kXStrideDw * g;
+  const uint32_t* xd = xg + kXHalfDw * h;   // inputs 60 h ..
+  uint32_t D[30];
+#pragma unroll
+  for (int q = 0; q < 7; ++q) {
+    const u4v v = *reinterpret_cast<const u4v*>(xd + 4 * q);
+    D[4 * q] = v.x;
+    D[4 * q + 1] = v.y;
+    D[4 * q + 2] = v.z;
+    D[4 * q + 3] = v.w;
+  }
+  const u2v b = *reinterpret_cast<const u2v*>(xd + 28);
+  D[28] = b.x;
+  D[29] = b.y;
+  const u2v t0 = *reinterpret_cast<const u2v*>(xg + kXTailDw);       // inputs 120..123
+  const u2v t1 = *reinterpret_cast<const u2v*>(xg + kXTailDw + 2);   // inputs 124..127
 #pragma unroll
   for (int m = 0; m < kHalfBytes / 2; ++m) {   // bytes 2m, 2m+1: inputs 10m .. 10m+9 = dwords 5m ..
-    const uint32_t d0 = xd[5 * m], d1 = xd[5 * m + 1], d2 = xd[5 * m + 2], d3 = xd[5 * m + 3], d4 = xd[5 * m + 4];
-    xr[5 * m] = d0;
-    xr[5 * m + 1] = d1;
+    const uint32_t d2 = D[5 * m + 2], d3 = D[5 * m + 3], d4 = D[5 * m + 4];
+    xr[5 * m] = D[5 * m];
+    xr[5 * m + 1] = D[5 * m + 1];
     xr[5 * m + 2] = __builtin_amdgcn_alignbit(d3, d2, 16);
     xr[5 * m + 3] = __builtin_amdgcn_alignbit(d4, d3, 16);
     xr[5 * m + 4] = __builtin_amdgcn_perm(d4, d2, 0x07060100u);   // (low half of d2, high half of d4)
   }
-  const uint16_t* xt = reinterpret_cast<const uint16_t*>(xsw + kXStrideDw * g) + 120 + 5 * h;
-  uint32_t e[5];
-#pragma unroll
-  for (int i = 0; i < 5; ++i) e[i] = (120 + 5 * h + i < kGroup) ? (uint32_t)xt[i] : 0u;
-  xr[30] = e[0] | (e[1] << 16);
-  xr[31] = e[2] | (e[3] << 16);
-  xr[32] = e[4];
+  // Half 0: (x120, x121), (x122, x123), (x124, 0).  Half 1: (x125, x126),
+  // (x127, 0), (0, 0).
+  xr[30] = h ? __builtin_amdgcn_alignbit(t1.y, t1.x, 16) : t0.x;
+  xr[31] = h ? t1.y >> 16 : t0.y;
+  xr[32] = h ? 0u : t1.x & 0xFFFFu;
 }
 
 // One pass of plane 0 for one lane: 12 body bytes, 1 tail byte, 1 scale.
@@ -329,10 +362,10 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   const int K = G * kGroup;
   uint32_t* xsw = reinterpret_cast<uint32_t*>(smem);
   // Plane-0 sum of every (row, wave of the row), then two values per record
-  // (its halves).  Pointers derive from the LDS base by plain offsets, so
-  // accesses stay LDS instructions.
+  // (its halves, 8-byte aligned).  Pointers derive from the LDS base by plain
+  // offsets, so accesses stay LDS instructions.
   float* rowsum = reinterpret_cast<float*>(smem + 4 * kXStrideDw * G);
-  float* recval = rowsum + rows_per_wg * segs;
+  float* recval = rowsum + ((rows_per_wg * segs + 1) & ~1);
   const int rec_cap = rows_per_wg * G;   // records a block can hold
 
   const int tid = threadIdx.x;
@@ -380,6 +413,11 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   // loads across these points (no instruction emitted).
   asm volatile("" ::: "memory");
   __builtin_amdgcn_sched_barrier(0);
+  // Every wave's x loads go out before any wave's weight loads: the CU
+  // serves its waves' loads in issue order, and x is needed first (a bare
+  // barrier, no wait for the loads).
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
   // 2. The block's record range: from the arguments with host ranges, else
   //    its first and last row pointers.  Without records x stands in as a
   //    readable address.
@@ -415,7 +453,11 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   if constexpr (kHostRanges) load_rec_half(rec, MR, rec_index(kr), has_rec ? hh : 0);
   asm volatile("" ::: "memory");
   __builtin_amdgcn_sched_barrier(0);
-  // 4. Every plane-0 pass of this lane.
+  // 4. The first kAhead plane-0 passes of this lane; each later pass is
+  //    issued once the pass kAhead before it has been computed.  Issuing
+  //    every pass here would stall the waves at issue (the CU holds only so
+  //    many loads in flight) and with them the set-up below.
+  constexpr int kAhead = kPasses < kPrefetch ? kPasses : kPrefetch;
   const uint32_t ngroups = (uint32_t)M.n_out * (uint32_t)G;
   const uint8_t* body0 = M.codes0 + kHalfBytes * h;
   const uint8_t* tail0 = M.codes0 + (size_t)(kMainBytes * ngroups) + h;
@@ -424,11 +466,12 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   const bool has_off = kOffset0 && M.offset0 != nullptr;
   const uint16_t* off0 = has_off ? M.offset0 : M.scale0;
   Pass buf[kPasses];
-#pragma unroll
-  for (int d = 0; d < kPasses; ++d) {
+  auto issue_pass = [&](int d) {
     const int r = min(row_begin + rl + d * ri, row_end - 1);
     load_pass<kOffset0>(buf[d], body0, tail0, M.scale0, off0, (uint32_t)r * (uint32_t)G + (uint32_t)g);
-  }
+  };
+#pragma unroll
+  for (int d = 0; d < kAhead; ++d) issue_pass(d);
   asm volatile("" ::: "memory");
   __builtin_amdgcn_sched_barrier(0);
   // 5. Thread t < nrb: the bounds of row t (it adds that row's records at
@@ -455,15 +498,16 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   }
 #pragma unroll
   for (int q = 0; q < kXLoads; ++q) {
-    // 8 halves: group i / 16, dwords 4 (i % 16) ..  Unconditional (threads
+    // 8 inputs 8c .. 8c + 7 of group i / 16 (c = i % 16), as two 4-input
+    // halves (neither straddles a part of the slot).  Unconditional (threads
     // past the end rewrite the last slot with the same data), so the load is
     // not sunk into a branch behind the weight loads.
+    typedef uint32_t u2v __attribute__((ext_vector_type(2)));
     const int i = min(tid + q * T, K / 8 - 1);
-    uint32_t* d = xsw + kXStrideDw * (i >> 4) + 4 * (i & 15);
-    d[0] = xv[q].x;
-    d[1] = xv[q].y;
-    d[2] = xv[q].z;
-    d[3] = xv[q].w;
+    const int c = i & 15;
+    uint32_t* xg = xsw + kXStrideDw * (i >> 4);
+    *reinterpret_cast<u2v*>(xg + x_slot_dw(8 * c)) = u2v{xv[q].x, xv[q].y};
+    *reinterpret_cast<u2v*>(xg + x_slot_dw(8 * c + 4)) = u2v{xv[q].z, xv[q].w};
   }
   __syncthreads();
 
@@ -492,6 +536,7 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
     // store below while their table reads cannot, and the reads' results of
     // every pass stay live at once.
     asm volatile("" : "+v"(v));
+    if (d + kAhead < kPasses) issue_pass(d + kAhead);
     v = (active && row < nrb) ? v : 0.f;
     const float sum = segment_sum(v, seg);
     if (in_rows && row < nrb && (sl & (seg - 1)) == seg - 1) rowsum[row * segs + (sl >> 6)] = sum;
@@ -514,17 +559,15 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
     float a = rowsum[tid * segs];
     for (int c = 1; c < segs; ++c) a += rowsum[tid * segs + c];
     if (has_rec) {
-      // Four records per step, loads first (absent ones add +0).
+      // Eight records per step, all reads first (absent ones add +0).
+      typedef float f2v __attribute__((ext_vector_type(2)));
       const int kb = max(rpa, k0), ke = min(min(rpz, k1), k0 + rec_cap);
-      for (int k = kb; k < ke; k += 4) {
-        float v[4];
+      for (int k = kb; k < ke; k += 8) {
+        f2v v[8];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int kk = min(k + u, ke - 1) - k0;
-          v[u] = recval[2 * kk] + recval[2 * kk + 1];
-        }
+        for (int u = 0; u < 8; ++u) v[u] = *reinterpret_cast<const f2v*>(recval + 2 * (min(k + u, ke - 1) - k0));
 #pragma unroll
-        for (int u = 0; u < 4; ++u) a += k + u < ke ? v[u] : 0.f;
+        for (int u = 0; u < 8; ++u) a += k + u < ke ? v[u].x + v[u].y : 0.f;
       }
     }
     store_y(yp, row_begin + tid, a, out_f32);
@@ -573,7 +616,7 @@ DeviceInfo& device_info() {
 size_t lds_bytes(int G, int rows) {
   const int SP = padded_slots(2 * G);
   const int segs = SP > 64 ? SP / 64 : 1;
-  return (size_t)kLutBytes + 4 * (size_t)kXStrideDw * G + 4 * (size_t)rows * segs + 8 * (size_t)rows * G;
+  return (size_t)kLutBytes + 4 * (size_t)kXStrideDw * G + 4 * (size_t)((rows * segs + 1) & ~1) + 8 * (size_t)rows * G;
 }
 
 }  // namespace
