@@ -43,10 +43,13 @@
 // * Plane 1.  Each record is handled by two threads (one per half).  A
 //   record half computes s1 * sum(t1 x) + mu * sum(x) over its half-group and
 //   stores it in its own LDS slot (records of a workgroup are contiguous in
-//   CSR order, so the slot is the record's index in that range).  Records
-//   are handled after plane 0.  When the host passes each workgroup's record
-//   range, their loads go out with the first batch; otherwise the range
-//   needs the row pointers first (one more memory round trip).
+//   CSR order, so the slot is the record's index in that range).  When the
+//   host passes each workgroup's record range, their loads go out with the
+//   first batch, and if extra waves (within 1024 threads) can take every
+//   record of a workgroup in one sweep, they do so while the other waves
+//   run plane 0.  Otherwise the plane-0 waves take the records after plane
+//   0 (without host ranges the range also needs the row pointers first, one
+//   more memory round trip).
 // * Reduction.  After each pass the lanes of a row add their plane-0 values
 //   with DPP (quad permutes, mirrors and row broadcasts folded into the
 //   adds); the last lane of each 64-lane segment writes the segment sum to
@@ -85,6 +88,9 @@ __device__ inline int x_slot_dw(int i) {
 constexpr int kMaxRangeEntries = 768;
 // Plane-0 passes whose loads are issued before the set-up.
 constexpr int kPrefetch = 2;
+// Most record sweeps a record wave may take (more sweeps measured slower:
+// the record waves then compete with plane 0 for the LDS).
+constexpr int kMaxRecSweeps = 1;
 
 static_assert(kRep == 16, "the table addressing assumes 16 copies");
 
@@ -344,12 +350,13 @@ __device__ inline void store_y(void* y, int i, float v, int out_f32) {
     reinterpret_cast<uint16_t*>(y)[i] = __builtin_bit_cast(uint16_t, (_Float16)v);
 }
 
-// kPasses: plane-0 passes per lane, all loaded up front.  kXLoads: 16-byte
+// kPasses: plane-0 passes per lane (the first kPrefetch loaded before the
+// set-up).  kXLoads: 16-byte
 // loads of x per thread (ceil(K / 8 / T)).  kHostRanges: the host passes
 // each workgroup's record range.
 template <int kPasses, int kXLoads, bool kHostRanges, bool kOffset0>
 __global__ void __launch_bounds__(kMaxThreads) __attribute__((amdgpu_waves_per_eu(4)))
-gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_per_wg, int32_t out_f32,
+gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_per_wg, int32_t opts,
             int32_t wb1, int32_t wb2, int32_t wb3, int32_t wb4, int32_t wb5, int32_t wb6, int32_t wb7,
             int32_t nthreads, const GemvArgs args) {
   // The table is the kernel's only static LDS, so it sits at LDS address 0
@@ -370,6 +377,10 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
 
   const int tid = threadIdx.x;
   const int T = nthreads;   // == blockDim.x, without a load of the dispatch packet
+  // opts: bit 0 fp32 output; bits 16.. the first thread of the record waves
+  // (0: no record waves, every thread takes records after plane 0).
+  const int out_f32 = opts & 1;
+  const int rec_tid0 = opts >> 16;
 
   // Which matrix this workgroup serves: the first workgroups of matrices
   // 1..7 arrive in SGPRs (unused ones are INT32_MAX), so the matrix record
@@ -433,9 +444,13 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   // Record halves: two consecutive threads per record, so that the record
   // work occupies as few waves as possible (the record code costs a wave
   // the same time however few of its lanes have a record).
-  const int hh = tid & 1;
-  const int kr = k0 + (tid >> 1);
-  const int per_sweep = T >> 1;
+  // With record waves (threads rec_tid0 .., whole waves) only they take
+  // records, from the start, while the other waves run plane 0.
+  const bool rec_wave = rec_tid0 > 0 && tid >= rec_tid0;
+  const int rt = rec_tid0 > 0 ? tid - rec_tid0 : tid;
+  const int hh = rt & 1;
+  const int kr = k0 + (rt >> 1);
+  const int per_sweep = (rec_tid0 > 0 ? T - rec_tid0 : T) >> 1;
   // Without records, plane-0 arrays stand in as readable addresses (the
   // loaded values are ignored).
   RecSrc MR;
@@ -527,6 +542,7 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   // Plane 0, one row per pass: s0 * sum_i t0 x over each half-group, summed
   // over the row's lanes of this wave.
   const int seg = SP < 64 ? SP : 64;
+  if (!rec_wave) {
 #pragma unroll
   for (int d = 0; d < kPasses; ++d) {
     const int row = rl + d * ri;
@@ -542,10 +558,11 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
     if (in_rows && row < nrb && (sl & (seg - 1)) == seg - 1) rowsum[row * segs + (sl >> 6)] = sum;
     __builtin_amdgcn_sched_barrier(0);   // keep passes apart: bounds the LUT reads in flight
   }
+  }
 
   // Plane 1: each record half stores its value (records of a block are
   // contiguous, so a record's slot is its index in the block).
-  if (has_rec) {
+  if (has_rec && (rec_tid0 == 0 || rec_wave)) {
     for (int k = kr, first = 1; k < k1; k += per_sweep, first = 0) {
       if (!kPreRec || !first) load_rec_half(rec, MR, rec_index(k), hh);
       if (k >= 0 && k - k0 < rec_cap) recval[2 * (k - k0) + hh] = record_half_value(lut, slot, xsw, rec, hh, G);
@@ -668,9 +685,6 @@ hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n, const uint16_t*
   const int ri = T / SP;
   const int passes = kPassChoices[pi];
   const int rows_per_wg = passes * ri;
-  const int xloads = (G * kGroup / 8 + T - 1) / T;
-  const int xi = xloads <= 1 ? 0 : (xloads <= 2 ? 1 : 2);
-  if (kXChoices[xi] < xloads) return hipErrorInvalidValue;
 
   GemvArgs A = {};
   int32_t wb[TQ_MAX_GROUPED];
@@ -717,6 +731,29 @@ hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n, const uint16_t*
     }
   }
 
+  // Record waves: with host ranges the largest record count of any
+  // workgroup is known, and extra waves (up to the 1024-thread limit) take
+  // the records while the others run plane 0, instead of the plane-0 waves
+  // taking them afterwards.  Used when they need at most kMaxRecSweeps
+  // sweeps.
+  int rec_threads = 0;
+  if (host_ranges) {
+    int maxrec = 0;
+    for (int i = 0; i < n; ++i) {
+      const int nwg = (ms[i].n_out + rows_per_wg - 1) / rows_per_wg;
+      const int32_t* t = A.rec_begin + A.m[i].wg_begin + i;
+      for (int j = 0; j < nwg; ++j) maxrec = t[j + 1] - t[j] > maxrec ? t[j + 1] - t[j] : maxrec;
+    }
+    const int want = (2 * maxrec + 63) / 64 * 64;
+    const int room = kMaxThreads - T;
+    if (want > 0 && room > 0 && (want + room - 1) / room <= kMaxRecSweeps) rec_threads = want < room ? want : room;
+  }
+  const int Tt = T + rec_threads;
+  const int xloads = (G * kGroup / 8 + Tt - 1) / Tt;
+  const int xi = xloads <= 1 ? 0 : (xloads <= 2 ? 1 : 2);
+  if (kXChoices[xi] < xloads) return hipErrorInvalidValue;
+  const int opts = (out_f32 ? 1 : 0) | (rec_threads > 0 ? T << 16 : 0);
+
   const int hr = host_ranges ? 1 : 0;
   bool any_off = false;
   for (int i = 0; i < n; ++i) any_off = any_off || ms[i].offset0 != nullptr;
@@ -732,8 +769,8 @@ hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n, const uint16_t*
     if (e != hipSuccess) return e;
     di.attr_set[hr][oi][pi][xi] = true;
   }
-  hipLaunchKernelGGL(kern, dim3(wg), dim3(T), lds_bytes(G, rows_per_wg) - kLutBytes, s, x, G, ri, rows_per_wg,
-                     out_f32 ? 1 : 0, wb[1], wb[2], wb[3], wb[4], wb[5], wb[6], wb[7], T, A);
+  hipLaunchKernelGGL(kern, dim3(wg), dim3(Tt), lds_bytes(G, rows_per_wg) - kLutBytes, s, x, G, ri, rows_per_wg,
+                     opts, wb[1], wb[2], wb[3], wb[4], wb[5], wb[6], wb[7], Tt, A);
   return hipGetLastError();
 }
 
