@@ -382,6 +382,16 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   const int out_f32 = opts & 1;
   const int rec_tid0 = opts >> 16;
 
+  // 1. x, first of all: it needs only preloaded arguments, so it goes out
+  //    before the wait for the matrix record below.
+  uint4 xv[kXLoads];
+#pragma unroll
+  for (int q = 0; q < kXLoads; ++q) xv[q] = reinterpret_cast<const uint4*>(x)[min(tid + q * T, K / 8 - 1)];
+  // Keep the issue order: neither the optimiser nor the scheduler may move
+  // loads across these points (no instruction emitted).
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+
   // Which matrix this workgroup serves: the first workgroups of matrices
   // 1..7 arrive in SGPRs (unused ones are INT32_MAX), so the matrix record
   // is one scalar load away.
@@ -397,6 +407,13 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
     hk0 = args.rec_begin[w + sel];
     hk1 = args.rec_begin[w + sel + 1];
   }
+  __builtin_amdgcn_sched_barrier(0);
+  // Every wave's x loads go out before any wave's weight loads: the CU
+  // serves its waves' loads in issue order, and x is needed first (a bare
+  // barrier, no wait for the loads; the record's scalar loads are already
+  // on their way).
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
   asm volatile("" ::"s"(M.codes0), "s"(M.scale0), "s"(M.rowptr1), "s"(M.gidx1), "s"(M.codes1), "s"(M.offset1),
                "s"(M.scale1), "s"(M.offset0), "s"(M.y), "s"(M.n_out), "s"(M.nnz1), "s"(M.wg_begin), "s"(hk0),
                "s"(hk1));
@@ -416,19 +433,6 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   const bool has_rec = M.nnz1 > 0;
 
   // Loads, in the order their data is needed (each wait is then exact).
-  // 1. x.
-  uint4 xv[kXLoads];
-#pragma unroll
-  for (int q = 0; q < kXLoads; ++q) xv[q] = reinterpret_cast<const uint4*>(x)[min(tid + q * T, K / 8 - 1)];
-  // Keep the issue order: neither the optimiser nor the scheduler may move
-  // loads across these points (no instruction emitted).
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_sched_barrier(0);
-  // Every wave's x loads go out before any wave's weight loads: the CU
-  // serves its waves' loads in issue order, and x is needed first (a bare
-  // barrier, no wait for the loads).
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_sched_barrier(0);
   // 2. The block's record range: from the arguments with host ranges, else
   //    its first and last row pointers.  Without records x stands in as a
   //    readable address.
@@ -483,7 +487,12 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   Pass buf[kPasses];
   auto issue_pass = [&](int d) {
     const int r = min(row_begin + rl + d * ri, row_end - 1);
-    load_pass<kOffset0>(buf[d], body0, tail0, M.scale0, off0, (uint32_t)r * (uint32_t)G + (uint32_t)g);
+    // Multiply, then add: fused into a 64-bit multiply-add, the unused high
+    // half of the addend can land on a register a load is still filling,
+    // and the wait for that load would stall the issue here.
+    uint32_t rg = (uint32_t)r * (uint32_t)G;
+    asm volatile("" : "+v"(rg));
+    load_pass<kOffset0>(buf[d], body0, tail0, M.scale0, off0, rg + (uint32_t)g);
   };
 #pragma unroll
   for (int d = 0; d < kAhead; ++d) issue_pass(d);
