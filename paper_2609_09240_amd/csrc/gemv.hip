@@ -451,7 +451,10 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   // With record waves (threads rec_tid0 .., whole waves) only they take
   // records, from the start, while the other waves run plane 0.
   const bool rec_wave = rec_tid0 > 0 && tid >= rec_tid0;
-  const int rt = rec_tid0 > 0 ? tid - rec_tid0 : tid;
+  // (Plane-0 threads of such a launch load the block's first record, which
+  // they never use: an index below the block's range would fetch other
+  // blocks' records for nothing.)
+  const int rt = rec_tid0 > 0 ? (rec_wave ? tid - rec_tid0 : 0) : tid;
   const int hh = rt & 1;
   const int kr = k0 + (rt >> 1);
   const int per_sweep = (rec_tid0 > 0 ? T - rec_tid0 : T) >> 1;
