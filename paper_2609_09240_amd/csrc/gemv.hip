@@ -208,6 +208,41 @@ __device__ __attribute__((always_inline)) inline float code_dot(const unsigned c
   return (a0 + a1) + a2;
 }
 
+// code_dot for kB activation rows at once: the table reads are shared, each
+// row keeps its own accumulators (same order as code_dot for each row).
+template <int kB>
+__device__ __attribute__((always_inline)) inline void code_dot_rows(const unsigned char* lut, uint32_t slot,
+                                                                   const uint32_t (&w)[4],
+                                                                   const uint32_t (&xr)[kB][kXrRegs],
+                                                                   float (&out)[kB]) {
+  typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+  float a0[kB], a1[kB], a2[kB];
+#pragma unroll
+  for (int b = 0; b < kB; ++b) a0[b] = a1[b] = a2[b] = 0.f;
+#pragma unroll
+  for (int m = 0; m < kHalfBytes / 2; ++m) {
+    const u4v e0 = *reinterpret_cast<const u4v*>(lut + code_addr(w, 2 * m, slot));
+    const u4v e1 = *reinterpret_cast<const u4v*>(lut + code_addr(w, 2 * m + 1, slot));
+    const uint32_t t4 = e0.z | e1.w;
+#pragma unroll
+    for (int b = 0; b < kB; ++b) {
+      a0[b] = fdot2(e0.x, xr[b][5 * m], a0[b]);
+      a1[b] = fdot2(e0.y, xr[b][5 * m + 1], a1[b]);
+      a0[b] = fdot2(e1.x, xr[b][5 * m + 2], a0[b]);
+      a1[b] = fdot2(e1.y, xr[b][5 * m + 3], a1[b]);
+      a2[b] = fdot2(t4, xr[b][5 * m + 4], a2[b]);
+    }
+  }
+  const U3 e = *reinterpret_cast<const U3*>(lut + code_addr(w, kHalfBytes, slot));
+#pragma unroll
+  for (int b = 0; b < kB; ++b) {
+    a0[b] = fdot2(e.x, xr[b][30], a0[b]);
+    a1[b] = fdot2(e.y, xr[b][31], a1[b]);
+    a2[b] = fdot2(e.z, xr[b][32], a2[b]);
+    out[b] = (a0[b] + a1[b]) + a2[b];
+  }
+}
+
 // Activations of half h of group g from the LDS copy of x: 12 body bytes
 // (inputs 60h + 5j ..) and the tail byte (inputs 120 + 5h ..); inputs past
 // the group (pad digits) are zero.  Seven 16-byte reads, one 8-byte read for
@@ -603,6 +638,212 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   }
 }
 
+// ------------------------------------------------------ a few batch rows
+// Y = X W^T for kB = 2..4 activation rows of one matrix: the GEMV above with
+// kB activation rows held in registers (33 each), so every code byte is
+// decoded once for all rows; for small batches this is cheaper than the
+// MFMA path (which must widen each code byte to 8 k-slots).  Records use the
+// host ranges and are taken by all threads after plane 0; X rows are staged
+// in LDS one after another.  Y is [kB][N].
+template <int kB>
+constexpr int batch_max_threads() {
+  return kB <= 2 ? 1024 : 512;   // 33 activation registers per row
+}
+
+template <int kPasses, int kXLoads, bool kOffset0, int kB>
+__global__ void __launch_bounds__(batch_max_threads<kB>())
+gemv_batch_kernel(const uint16_t* __restrict__ X, int32_t G, int32_t ri, int32_t rows_per_wg, int32_t out_f32,
+                  int32_t rec_slots, int32_t nthreads, const GemvArgs args) {
+  __shared__ __attribute__((aligned(16))) unsigned char lut[kLutBytes];
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int S = 2 * G;
+  const int SP = padded_slots(S);
+  const int segs = SP > 64 ? SP >> 6 : 1;
+  const int K = G * kGroup;
+  const int xslot = kXStrideDw * G;   // dwords per staged X row
+  uint32_t* xsw = reinterpret_cast<uint32_t*>(smem);
+  // Wave sums [row][wave of the row][batch row], then record values
+  // [record][half][batch row].
+  float* rowsum = reinterpret_cast<float*>(smem + 4 * (size_t)xslot * kB);
+  float* recval = rowsum + ((rows_per_wg * segs * kB + 1) & ~1);
+  const int tid = threadIdx.x;
+  const int T = nthreads;
+
+  // 1. X, first of all.
+  uint4 xv[kB][kXLoads];
+#pragma unroll
+  for (int b = 0; b < kB; ++b)
+#pragma unroll
+    for (int q = 0; q < kXLoads; ++q)
+      xv[b][q] = reinterpret_cast<const uint4*>(X + (size_t)b * K)[min(tid + q * T, K / 8 - 1)];
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  const int w = blockIdx.x;
+  const GemvMat M = args.m[0];
+  const int hk0 = args.rec_begin[w], hk1 = args.rec_begin[w + 1];
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("" ::"s"(M.codes0), "s"(M.scale0), "s"(M.rowptr1), "s"(M.gidx1), "s"(M.codes1), "s"(M.offset1),
+               "s"(M.scale1), "s"(M.offset0), "s"(M.y), "s"(M.n_out), "s"(M.nnz1), "s"(hk0), "s"(hk1));
+  __builtin_amdgcn_sched_barrier(0);
+  const int row_begin = w * rows_per_wg;
+  const int row_end = min(M.n_out, row_begin + rows_per_wg);
+  const int nrb = row_end - row_begin;
+
+  const bool in_rows = tid < ri * SP;
+  const int sl = in_rows ? tid % SP : 0;
+  const bool active = in_rows && sl < S;
+  const int g = active ? sl >> 1 : 0;
+  const int h = sl & 1;
+  const int rl = in_rows ? tid / SP : 0;
+  const uint32_t slot = (uint32_t)(tid & (kRep - 1)) << 4;
+  const bool has_rec = M.nnz1 > 0;
+
+  // 2. Records of this block (host ranges), first sweep.
+  const int k0 = hk0, k1 = hk1;
+  const int hh = tid & 1;
+  const int kr = k0 + (tid >> 1);
+  const int per_sweep = T >> 1;
+  RecSrc MR;
+  MR.codes1 = has_rec ? M.codes1 : M.codes0;
+  MR.nnz1 = has_rec ? (uint32_t)M.nnz1 : 0u;
+  MR.gidx1 = has_rec ? M.gidx1 : M.scale0;
+  MR.offset1 = has_rec ? M.offset1 : M.scale0;
+  MR.scale1 = has_rec ? M.scale1 : M.scale0;
+  const int kmax = has_rec ? M.nnz1 - 1 : 0;
+  RecHalf rec;
+  auto rec_index = [&](int k) -> uint32_t { return (uint32_t)max(min(k, min(max(k1 - 1, k0), kmax)), 0); };
+  load_rec_half(rec, MR, rec_index(kr), has_rec ? hh : 0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  // 3. The first passes of plane 0; later ones inside the pass loop.
+  constexpr int kAhead = kPasses < kPrefetch ? kPasses : kPrefetch;
+  const uint32_t ngroups = (uint32_t)M.n_out * (uint32_t)G;
+  const uint8_t* body0 = M.codes0 + kHalfBytes * h;
+  const uint8_t* tail0 = M.codes0 + (size_t)(kMainBytes * ngroups) + h;
+  const bool has_off = kOffset0 && M.offset0 != nullptr;
+  const uint16_t* off0 = has_off ? M.offset0 : M.scale0;
+  Pass buf[kPasses];
+  auto issue_pass = [&](int d) {
+    const int r = min(row_begin + rl + d * ri, row_end - 1);
+    uint32_t rg = (uint32_t)r * (uint32_t)G;
+    asm volatile("" : "+v"(rg));
+    load_pass<kOffset0>(buf[d], body0, tail0, M.scale0, off0, rg + (uint32_t)g);
+  };
+#pragma unroll
+  for (int d = 0; d < kAhead; ++d) issue_pass(d);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  // 4. Row bounds for the row totals.
+  const int* rpb = has_rec ? M.rowptr1 + row_begin : reinterpret_cast<const int*>(X);
+  const int tr = has_rec ? min(tid, nrb - 1) : 0;
+  const int rpa = rpb[tr];
+  const int rpz = rpb[has_rec ? tr + 1 : 0];
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+
+  // Set-up: the table, then the X rows.
+  for (int c = tid; c < 256; c += T) {
+    const uint4 e = lut_entry(c);
+#pragma unroll
+    for (int q = 0; q < kRep; ++q) reinterpret_cast<uint4*>(lut)[c * kRep + ((q + c) & (kRep - 1))] = e;
+  }
+#pragma unroll
+  for (int b = 0; b < kB; ++b) {
+#pragma unroll
+    for (int q = 0; q < kXLoads; ++q) {
+      typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+      const int i = min(tid + q * T, K / 8 - 1);
+      const int c = i & 15;
+      uint32_t* xg = xsw + xslot * b + kXStrideDw * (i >> 4);
+      *reinterpret_cast<u2v*>(xg + x_slot_dw(8 * c)) = u2v{xv[b][q].x, xv[b][q].y};
+      *reinterpret_cast<u2v*>(xg + x_slot_dw(8 * c + 4)) = u2v{xv[b][q].z, xv[b][q].w};
+    }
+  }
+  __syncthreads();
+
+  uint32_t xr[kB][kXrRegs];
+#pragma unroll
+  for (int b = 0; b < kB; ++b) load_xr(xr[b], xsw + xslot * b, g, h);
+  float xsum[kB];
+#pragma unroll
+  for (int b = 0; b < kB; ++b) {
+    xsum[b] = 0.f;
+    if constexpr (kOffset0) {
+      typedef _Float16 h2v __attribute__((ext_vector_type(2)));
+      const h2v ones = {(_Float16)1.0f, (_Float16)1.0f};
+#pragma unroll
+      for (int i = 0; i < kXrRegs; ++i)
+        xsum[b] = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2v, xr[b][i]), ones, xsum[b], false);
+    }
+  }
+
+  // Plane 0.
+  const int seg = SP < 64 ? SP : 64;
+#pragma unroll
+  for (int d = 0; d < kPasses; ++d) {
+    const int row = rl + d * ri;
+    float v[kB];
+    code_dot_rows<kB>(lut, slot, buf[d].w, xr, v);
+    const float sc = h2f(buf[d].sc);
+#pragma unroll
+    for (int b = 0; b < kB; ++b) {
+      v[b] = v[b] * sc;
+      if constexpr (kOffset0) v[b] = v[b] + (has_off ? h2f(buf[d].mu) : 0.f) * xsum[b];
+      asm volatile("" : "+v"(v[b]));
+    }
+    if (d + kAhead < kPasses) issue_pass(d + kAhead);
+#pragma unroll
+    for (int b = 0; b < kB; ++b) {
+      const float vb = (active && row < nrb) ? v[b] : 0.f;
+      const float sum = segment_sum(vb, seg);
+      if (in_rows && row < nrb && (sl & (seg - 1)) == seg - 1) rowsum[(row * segs + (sl >> 6)) * kB + b] = sum;
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // Plane 1, all threads, sweeps of T / 2 records.
+  if (has_rec) {
+    for (int k = kr, first = 1; k < k1; k += per_sweep, first = 0) {
+      if (!first) load_rec_half(rec, MR, rec_index(k), hh);
+      if (k >= 0 && k - k0 < rec_slots) {
+        uint32_t xq[kB][kXrRegs];
+        const int rg = min((int)rec.g, G - 1);
+#pragma unroll
+        for (int b = 0; b < kB; ++b) load_xr(xq[b], xsw + xslot * b, rg, hh);
+        float p[kB];
+        code_dot_rows<kB>(lut, slot, rec.w, xq, p);
+#pragma unroll
+        for (int b = 0; b < kB; ++b) {
+          float s0 = 0.f, s1 = 0.f, s2 = 0.f;
+#pragma unroll
+          for (int i = 0; i < kXrRegs; i += 3) {
+            s0 = fdot2(xq[b][i], 0x3C003C00u, s0);
+            s1 = fdot2(xq[b][i + 1], 0x3C003C00u, s1);
+            s2 = fdot2(xq[b][i + 2], 0x3C003C00u, s2);
+          }
+          const float xs = (s0 + s1) + s2;
+          recval[(2 * (k - k0) + hh) * kB + b] = h2f(rec.s1) * p[b] + h2f(rec.mu) * xs;
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // Row totals, one thread per row, every batch row in a fixed order.
+  if (tid < nrb) {
+    const int kb = has_rec ? max(rpa, k0) : 0, ke = has_rec ? min(min(rpz, k1), k0 + rec_slots) : 0;
+#pragma unroll
+    for (int b = 0; b < kB; ++b) {
+      float a = rowsum[(tid * segs) * kB + b];
+      for (int c = 1; c < segs; ++c) a += rowsum[(tid * segs + c) * kB + b];
+      for (int k = kb; k < ke; ++k) a += recval[(2 * (k - k0)) * kB + b] + recval[(2 * (k - k0) + 1) * kB + b];
+      store_y(M.y, b * M.n_out + row_begin + tid, a, out_f32);
+    }
+  }
+}
+
 typedef void (*GemvKernel)(const uint16_t*, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t,
                            int32_t, int32_t, int32_t, int32_t, const GemvArgs);
 
@@ -783,6 +1024,160 @@ hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n, const uint16_t*
   }
   hipLaunchKernelGGL(kern, dim3(wg), dim3(Tt), lds_bytes(G, rows_per_wg) - kLutBytes, s, x, G, ri, rows_per_wg,
                      opts, wb[1], wb[2], wb[3], wb[4], wb[5], wb[6], wb[7], Tt, A);
+  return hipGetLastError();
+}
+
+namespace {
+
+typedef void (*BatchKernel)(const uint16_t*, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t, const GemvArgs);
+
+template <int PI, int XI, bool OFF, int B>
+constexpr BatchKernel batch_kernel_at() {
+  return gemv_batch_kernel<kPassChoices[PI], kXChoices[XI], OFF, B>;
+}
+
+template <bool OFF, int B>
+BatchKernel select_batch(int pi, int xi) {
+  static const BatchKernel table[kNumPass][3] = {
+      {batch_kernel_at<0, 0, OFF, B>(), batch_kernel_at<0, 1, OFF, B>(), batch_kernel_at<0, 2, OFF, B>()},
+      {batch_kernel_at<1, 0, OFF, B>(), batch_kernel_at<1, 1, OFF, B>(), batch_kernel_at<1, 2, OFF, B>()},
+      {batch_kernel_at<2, 0, OFF, B>(), batch_kernel_at<2, 1, OFF, B>(), batch_kernel_at<2, 2, OFF, B>()},
+      {batch_kernel_at<3, 0, OFF, B>(), batch_kernel_at<3, 1, OFF, B>(), batch_kernel_at<3, 2, OFF, B>()},
+      {batch_kernel_at<4, 0, OFF, B>(), batch_kernel_at<4, 1, OFF, B>(), batch_kernel_at<4, 2, OFF, B>()},
+      {batch_kernel_at<5, 0, OFF, B>(), batch_kernel_at<5, 1, OFF, B>(), batch_kernel_at<5, 2, OFF, B>()},
+  };
+  return table[pi][xi];
+}
+
+struct BatchDeviceInfo {
+  int cus = 0;
+  bool attr_set[2][3][kNumPass][3] = {};
+};
+
+BatchDeviceInfo& batch_device_info() {
+  static thread_local BatchDeviceInfo info[64];
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  return info[dev & 63];
+}
+
+size_t batch_lds_bytes(int G, int B, int rows, int rec_slots) {
+  const int SP = padded_slots(2 * G);
+  const int segs = SP > 64 ? SP / 64 : 1;
+  return (size_t)kLutBytes + 4 * (size_t)kXStrideDw * G * B + 4 * (size_t)((rows * segs * B + 1) & ~1) +
+         8 * (size_t)B * rec_slots;
+}
+
+}  // namespace
+
+bool gemv_batch_supported(const MatDev& m, int B) {
+  return B >= 2 && B <= 4 && (m.nnz1 == 0 || m.rowptr1_host != nullptr);
+}
+
+hipError_t launch_gemv_batch(const MatDev& m, const uint16_t* X, int B, void* Y, bool out_f32, hipStream_t s) {
+  if (!gemv_batch_supported(m, B)) return hipErrorNotSupported;
+  BatchDeviceInfo& di = batch_device_info();
+  if (di.cus == 0) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    e = hipDeviceGetAttribute(&di.cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+  }
+  const int G = m.n_groups;
+  const int SP = padded_slots(2 * G);
+  const int tmax = B <= 2 ? 1024 : 512;
+  // Records per workgroup for a given row count, from the host row pointers.
+  auto max_records = [&](int rows) -> int {
+    if (m.nnz1 == 0) return 0;
+    int best = 0;
+    for (int64_t r = 0; r < m.n_out; r += rows) {
+      const int64_t e = r + rows < m.n_out ? r + rows : m.n_out;
+      const int64_t c = (int64_t)m.rowptr1_host[e] - m.rowptr1_host[r];
+      best = c > best ? (int)c : best;
+    }
+    return best;
+  };
+  // The GEMV's launch policy (one round of workgroups, then the fewest rows,
+  // then the fewest waves + 4 * passes), within this kernel's LDS.
+  int T = 0, pi = -1, rec_slots = 0;
+  int64_t best_rounds = 0;
+  int best_rows = 0, best_score = 0;
+  for (int t = 256; t <= tmax; t += 64) {
+    if (t % SP != 0 || (G * kGroup / 8 + t - 1) / t > kXChoices[2]) continue;
+    const int r = t / SP;
+    for (int p = 0; p < kNumPass; ++p) {
+      const int rows = kPassChoices[p] * r;
+      if (rows > t) break;
+      const int64_t nwg = (m.n_out + rows - 1) / rows;
+      if (nwg + 1 > kMaxRangeEntries) continue;
+      const int mr = max_records(rows);
+      if (batch_lds_bytes(G, B, rows, mr > 0 ? mr : 1) > 160 * 1024) break;
+      const int64_t rounds = (nwg + di.cus - 1) / di.cus;
+      const int score = t / 64 + 4 * kPassChoices[p];
+      if (pi < 0 || rounds < best_rounds ||
+          (rounds == best_rounds && (rows < best_rows || (rows == best_rows && score < best_score)))) {
+        T = t;
+        pi = p;
+        rec_slots = mr > 0 ? mr : 1;
+        best_rounds = rounds;
+        best_rows = rows;
+        best_score = score;
+      }
+    }
+  }
+  if (pi < 0) {
+    // Four rows whose staged x does not fit beside the table: two launches
+    // of two rows each (still one decode per code byte per pair of rows).
+    if (B != 4) return hipErrorNotSupported;
+    const size_t yb = (out_f32 ? 4 : 2) * (size_t)m.n_out;
+    hipError_t e = launch_gemv_batch(m, X, 2, Y, out_f32, s);
+    if (e != hipSuccess) return e;
+    return launch_gemv_batch(m, X + 2 * (size_t)G * kGroup, 2, static_cast<char*>(Y) + 2 * yb, out_f32, s);
+  }
+  const int ri = T / SP;
+  const int rows_per_wg = kPassChoices[pi] * ri;
+  const int xloads = (G * kGroup / 8 + T - 1) / T;
+  const int xi = xloads <= 1 ? 0 : (xloads <= 2 ? 1 : 2);
+  const int nwg = (int)((m.n_out + rows_per_wg - 1) / rows_per_wg);
+
+  GemvArgs A = {};
+  GemvMat& a = A.m[0];
+  a.codes0 = m.codes0;
+  a.scale0 = m.scale0;
+  a.rowptr1 = m.rowptr1;
+  a.gidx1 = m.gidx1;
+  a.codes1 = m.codes1;
+  a.offset1 = m.offset1;
+  a.scale1 = m.scale1;
+  a.offset0 = m.offset0;
+  a.y = Y;
+  a.n_out = m.n_out;
+  a.nnz1 = (int32_t)m.nnz1;
+  a.wg_begin = 0;
+  for (int j = 0; j <= nwg; ++j) {
+    int64_t v = 0;
+    if (m.nnz1 > 0) {
+      const int64_t r = (int64_t)j * rows_per_wg < m.n_out ? (int64_t)j * rows_per_wg : m.n_out;
+      v = m.rowptr1_host[r];
+      v = v < 0 ? 0 : (v > m.nnz1 ? m.nnz1 : v);
+    }
+    A.rec_begin[j] = (int32_t)v;
+  }
+  const bool off = m.offset0 != nullptr;
+  BatchKernel kern;
+  if (B == 2) kern = off ? select_batch<true, 2>(pi, xi) : select_batch<false, 2>(pi, xi);
+  else if (B == 3) kern = off ? select_batch<true, 3>(pi, xi) : select_batch<false, 3>(pi, xi);
+  else kern = off ? select_batch<true, 4>(pi, xi) : select_batch<false, 4>(pi, xi);
+  bool& set = di.attr_set[off ? 1 : 0][B - 2][pi][xi];
+  if (!set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - kLutBytes);
+    if (e != hipSuccess) return e;
+    set = true;
+  }
+  hipLaunchKernelGGL(kern, dim3(nwg), dim3(T), batch_lds_bytes(G, B, rows_per_wg, rec_slots) - kLutBytes, s, X, G,
+                     ri, rows_per_wg, out_f32 ? 1 : 0, rec_slots, T, A);
   return hipGetLastError();
 }
 

@@ -159,6 +159,12 @@ tq_status tq_gemm_smallbatch(const tq_matrix* m, const uint16_t* X, int32_t B, v
     void* ys[1] = {Y};
     return from_hip(tq::launch_gemv(&d, ys, 1, X, flags == TQ_OUT_FP32, (hipStream_t)stream));
   }
+  if (tq::gemv_batch_supported(d, B)) {
+    // A few rows: the GEMV's decode with one accumulator set per row, where
+    // its launch fits; otherwise the MFMA path below.
+    const hipError_t e = tq::launch_gemv_batch(d, X, B, Y, flags == TQ_OUT_FP32, (hipStream_t)stream);
+    if (e != hipErrorNotSupported) return from_hip(e);
+  }
   return from_hip(tq::launch_gemm_smallbatch(d, X, B, Y, flags == TQ_OUT_FP32, (hipStream_t)stream));
 }
 

@@ -44,6 +44,12 @@ hipError_t launch_unpack_fp16(const MatDev& m, uint16_t* w, hipStream_t s);
 hipError_t launch_gemv(const MatDev* ms, void* const* ys, int n,
                        const uint16_t* x, bool out_f32, hipStream_t s);
 
+// A few batch rows (2..4) through the GEMV's decode, each code byte decoded
+// once for all rows; needs the host row pointers when the matrix has
+// records.  Returns hipErrorNotSupported where it does not apply.
+bool gemv_batch_supported(const MatDev& m, int B);
+hipError_t launch_gemv_batch(const MatDev& m, const uint16_t* X, int B, void* Y, bool out_f32, hipStream_t s);
+
 hipError_t launch_gemm_smallbatch(const MatDev& m, const uint16_t* X, int B,
                                   void* Y, bool out_f32, hipStream_t s);
 

@@ -89,3 +89,63 @@ def test_group_offsets(B, n_out, n_in, f2):
     got = run(case, X, out_f32=True)
     r = assert_within_bound(got, case.oracle_gemm(X), case.bound(X), f"offsets B={B} {n_out}x{n_in}")
     log(f"  max err/bound {r:.3g}")
+
+
+# --------------------------------------- B = 2..4: the GEMV decode per row
+
+@pytest.mark.parametrize("B", [2, 3, 4])
+@pytest.mark.parametrize("n_out,n_in,f2", [
+    (12288, 4096, 0.1), (4096, 12288, 0.1), (1024, 4096, 0.1), (3000, 640, 0.1), (65, 384, 0.5),
+    (1, 128, 1.0), (257, 128, 0.0), (100, 32768, 0.05),
+])
+def test_few_rows_match_oracle_and_mfma_path(B, n_out, n_in, f2):
+    """B = 2..4 decode each code byte once for every row (the GEMV's table
+    and layout) where the launch fits, the MFMA path otherwise (K = 32768 at
+    B = 3, 4, or no host row pointers): both within the bound everywhere."""
+    inp = synth.linear(n_out, n_in, f2, (21, n_out, n_in, B))
+    X = synth.activations(n_in, (21, n_out, n_in, 98), batch=B, outlier_frac=0.01)
+    case = Case(inp)
+    got = run(case, X, out_f32=True)
+    want = case.oracle_gemm(X)
+    r = assert_within_bound(got, want, case.bound(X), f"few rows B={B} {n_out}x{n_in}")
+    mfma = run(Case(inp, host_rowptr=False), X, out_f32=True)
+    r2 = assert_within_bound(mfma, want, case.bound(X), f"mfma B={B} {n_out}x{n_in}")
+    log(f"few rows B={B} {n_out}x{n_in}: max err/bound {r:.3g} (mfma path {r2:.3g})")
+
+
+@pytest.mark.parametrize("name,B", [
+    ("q", 2), ("q", 3), ("q", 4), ("k", 2), ("k", 4), ("gate", 2), ("gate", 3), ("gate", 4), ("down", 2), ("down", 3),
+    ("down", 4),
+])
+def test_few_rows_equal_gemv_per_row(name, B):
+    """Each row of a B = 2..4 batch goes through the same arithmetic, in the
+    same order, as the GEMV of that row alone: equal values (+0 and -0
+    compare equal), fp16 and fp32 outputs.  (down at B = 4 runs as two
+    launches of two rows: four staged rows of x do not fit in LDS beside the
+    table.)"""
+    case = Case(synth.projection(name, layer=1, cfg=4))
+    X = synth.stage_activations(synth.STAGE_OF[name], layer=1, cfg=4, batch=B)
+    for out_f32 in (False, True):
+        Y = run(case, X, out_f32=out_f32)
+        for b in range(B):
+            y = tq.tq_gemv(case.gpu, torch.from_numpy(X[b].copy()).cuda(), out_f32=out_f32)
+            torch.cuda.synchronize()
+            assert np.array_equal(Y[b], y.cpu().numpy()), f"{name} B={B} row {b} f32={out_f32}"
+    want = case.oracle_gemm(X)
+    r = assert_within_bound(run(case, X, True), want, case.bound(X), f"{name} B={B}")
+    log(f"few rows {name} B={B}: equal to the GEMV per row, max err/bound {r:.3g}")
+
+
+@pytest.mark.parametrize("B", [2, 3, 4])
+@pytest.mark.parametrize("n_out,n_in,f2", [(4096, 4096, synth.PAPER_TWO_PLANE), (300, 1024, 0.1)])
+def test_few_rows_group_offsets(B, n_out, n_in, f2):
+    inp = synth.linear(n_out, n_in, f2, (23, n_out, n_in, B), offset0=True)
+    X = synth.activations(n_in, (23, n_out, n_in, 97), batch=B, outlier_frac=0.01)
+    case = Case(inp)
+    got = run(case, X, out_f32=True)
+    r = assert_within_bound(got, case.oracle_gemm(X), case.bound(X), f"few rows offsets B={B}")
+    for b in range(B):
+        y = tq.tq_gemv(case.gpu, torch.from_numpy(X[b].copy()).cuda(), out_f32=True)
+        torch.cuda.synchronize()
+        assert np.array_equal(got[b], y.cpu().numpy())
+    log(f"few rows offsets B={B} {n_out}x{n_in}: max err/bound {r:.3g}")
