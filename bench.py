@@ -117,7 +117,20 @@ def time_stack(mats, xs, steps, warmup):
             graph.replay()
         t_stop.record(stream)
     torch.cuda.synchronize()
-    return t_start.elapsed_time(t_stop) / steps, launches, graph, outs
+    ms_per_step = t_start.elapsed_time(t_stop) / steps
+    # Spread: the same number of replays again, each between its own pair
+    # of events (outside the timed region above).
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    with torch.cuda.stream(stream):
+        for a, b in evs:
+            a.record(stream)
+            graph.replay()
+            b.record(stream)
+    torch.cuda.synchronize()
+    per_step = sorted(a.elapsed_time(b) * 1e3 for a, b in evs)
+    time_stack.spread_us = {q: round(per_step[min(len(per_step) - 1, int(q / 100 * len(per_step)))], 2)
+                            for q in (10, 50, 90)}
+    return ms_per_step, launches, graph, outs
 
 
 def algorithmic_bytes(launches):
@@ -422,6 +435,7 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 6),
         "us_per_step": round(ms_per_step * 1e3, 2),
+        "step_us_p10_p50_p90": [time_stack.spread_us[q] for q in (10, 50, 90)],
         "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
         "pct_of_stream_ceiling": round(100 * gbs / ceiling["GBps"], 2),
         "stream_ceiling": ceiling,
