@@ -350,6 +350,21 @@ __device__ __attribute__((always_inline)) inline float record_half_value(const u
   return h2f(r.s1) * p1 + h2f(r.mu) * xsum;
 }
 
+// Wave priority for plane-0 pass d of n: high for early passes, falling to
+// 0 for the last.  The CU issues for its oldest waves first, so without it
+// the youngest waves of a workgroup start their passes last and finish
+// long after the others, with fewer and fewer waves left to keep the LDS
+// busy; by pass, the waves that are behind are served first.
+template <int kPasses>
+__device__ __attribute__((always_inline)) inline void pass_priority(int d) {
+  switch ((kPasses - 1 - d) * 4 / kPasses) {
+    case 3: __builtin_amdgcn_s_setprio(3); break;
+    case 2: __builtin_amdgcn_s_setprio(2); break;
+    case 1: __builtin_amdgcn_s_setprio(1); break;
+    default: __builtin_amdgcn_s_setprio(0); break;
+  }
+}
+
 // Sum of v over aligned segments of seg lanes (seg a power of two <= 64),
 // exact in the last lane of each segment (and in every lane for seg <= 16).
 // Butterflies inside 16-lane rows, then row broadcasts: a fixed order, so
@@ -593,6 +608,7 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
 #pragma unroll
   for (int d = 0; d < kPasses; ++d) {
     const int row = rl + d * ri;
+    pass_priority<kPasses>(d);
     float v = code_dot(lut, slot, buf[d].w, xr) * h2f(buf[d].sc);
     if constexpr (kOffset0) v = v + (has_off ? h2f(buf[d].mu) : 0.f) * xsum;
     // Pin the value here: otherwise the dot products sink into the guarded
@@ -607,6 +623,7 @@ gemv_kernel(const uint16_t* __restrict__ x, int32_t G, int32_t ri, int32_t rows_
   }
   }
 
+  __builtin_amdgcn_s_setprio(0);
   // Plane 1: each record half stores its value (records of a block are
   // contiguous, so a record's slot is its index in the block).
   if (has_rec && (rec_tid0 == 0 || rec_wave)) {
@@ -784,6 +801,7 @@ gemv_batch_kernel(const uint16_t* __restrict__ X, int32_t G, int32_t ri, int32_t
 #pragma unroll
   for (int d = 0; d < kPasses; ++d) {
     const int row = rl + d * ri;
+    pass_priority<kPasses>(d);
     float v[kB];
     code_dot_rows<kB>(lut, slot, buf[d].w, xr, v);
     const float sc = h2f(buf[d].sc);
@@ -803,6 +821,7 @@ gemv_batch_kernel(const uint16_t* __restrict__ X, int32_t G, int32_t ri, int32_t
     __builtin_amdgcn_sched_barrier(0);
   }
 
+  __builtin_amdgcn_s_setprio(0);
   // Plane 1, all threads, sweeps of T / 2 records.
   if (has_rec) {
     for (int k = kr, first = 1; k < k1; k += per_sweep, first = 0) {
