@@ -6,28 +6,32 @@
 // v_mfma_f32_16x16x32_f16: A = 16 weight rows, B = 16 batch rows, C = the
 // 16 x 16 block of Y^T.
 //
-// Slot order.  MFMA sums over k in any order.  Each group's 128 inputs are
-// laid out as 28 code bytes (26 real, 2 pad) of 8 slots each: byte j owns
-// slots 8j .. 8j+7 holding inputs 5j .. 5j+4 and three zeros, so one MFMA
-// k-step (32 slots) covers bytes 4s .. 4s+3 and lane block q of the A
-// operand decodes exactly one code byte (4s + q).  The B operand gathers the
-// same five activations from X (one 12-byte load, a half-word shift for odd
-// bytes) and zeros the pad slots, so the slot order never reaches memory.
+// k order.  MFMA sums over k in any order, so the 32 k of a step are chosen
+// to make both operands cheap.  Groups are taken four at a time (a quad);
+// lane block q (lanes 16q .. 16q+15) works on group 4Q + q in every step of
+// quad Q, and step u (0..15) takes inputs 8u .. 8u+7 of each block's group.
+// The B operand is then one aligned 16-byte chunk of X per lane, and the
+// code bytes and trit phase of a window (its first input is trit 8u % 5 of
+// byte 8u / 5) are fixed per step, known at compile time.
 //
-// Decode.  A code byte maps through an LDS table to five v_perm selectors;
-// v_perm then picks each weight's fp16 bits from {-s0, +0, +s0} (plane 0)
-// or {mu - s1, mu, mu + s1} (plane 1, rounded to fp16 once per record), so a
-// weight costs no arithmetic.  On two-plane groups the two halves are added
-// in fp16 (one more rounding; the result stays within the accuracy bound).
+// Decode.  The GEMV's table (fp16 +-1/0 patterns (t0,t1), (t2,t3), (t4,0)
+// per code, 16 copies, at LDS address 0) is read once per code byte (a
+// byte shared by two windows is kept in registers); a window's four dwords
+// are table dwords or two of them joined by v_alignbit / v_lshl_or.  A
+// weight is pattern * s0 + offset in one v_pk_fma_f16 (exact without
+// offsets); on two-plane groups the plane-1 pattern * s1 is added with one
+// more fma and the record's offset is folded into the plane-0 term, so a
+// weight takes at most three fp16 roundings (well inside the accuracy
+// bound).
 //
-// Staging.  A workgroup owns 16 RT consecutive weight rows.  Their packed
-// bytes (one contiguous span per buffer), scales and plane-1 records are
-// loaded in one burst of coalesced loads and written to LDS as one 32-byte
-// slot per (group, row).  Waves then own (row tile, K quarter) pairs; when a
-// workgroup has fewer row tiles than waves, K is split across waves and the
-// partial sums are added in a fixed order through LDS (bit-reproducible).
-// Shapes whose staging does not fit (more than kMaxPairs (row, group) pairs
-// per row tile) use the simple per-group kernel at the end of this file.
+// Work split.  A workgroup of 8 waves owns 16 RT consecutive rows.  Its
+// waves split K by quads, and each wave covers all RT row tiles and all
+// batch columns, so a CU reads its slice of X once and decodes every weight
+// once.  Plane-0 codes go straight to registers, all loaded up front; X is
+// loaded a few pairs ahead of use.  The workgroup's plane-1 records are
+// staged in LDS with one slot per (row, group).  The waves' partial sums are
+// added in a fixed order through LDS (bit-reproducible).  Shapes beyond the
+// staging limits use the simple per-group kernel at the end of this file.
 
 #include "tq_internal.h"
 
@@ -39,21 +43,23 @@ typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef float float4v __attribute__((ext_vector_type(4)));
 typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 
-constexpr int kLutCopies = 8;                       // table copies (lane & 7)
-constexpr int kLutEntries = 256;
-constexpr int kMaxPairs = 1536;                     // staged (row, group) pairs per workgroup
-constexpr int kSlotBytes = 32;
-constexpr int kStepsPerGroup = 7;                   // 28 code bytes / 4 per k-step
-constexpr int kRecBatch = 2;                        // plane-1 records loaded per thread per batch
 constexpr int kLdsLimit = 160 * 1024;
-constexpr int kLutBytes = kLutEntries * kLutCopies * 16;
+constexpr int kQWaves = 8;                       // waves per workgroup (K split)
+constexpr int kQThreads = 64 * kQWaves;
+constexpr int kQRep = 16;                        // table copies (lane & 15)
+constexpr int kQLutBytes = 256 * kQRep * 16;     // 64 KiB at LDS address 0
+constexpr int kQMaxPairs = 2048;                 // record slots (rows x groups) per workgroup
+constexpr int kQMaxUnits = 4;                    // row tiles x quads per wave
+constexpr int kWindows = 16;                     // 8-input k blocks per group
 
-// Dynamic LDS bytes for P staged pairs and R rows.
-__host__ __device__ constexpr int staged_bytes(int P, int R) {
-  return P * (2 * kSlotBytes + 2 + 2 + 1) + 4 * (R + 1);
-}
+__device__ inline float h2f(uint32_t b) { return (float)__builtin_bit_cast(_Float16, (uint16_t)b); }
+__device__ inline uint32_t f2h(float a) { return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)a); }
 
-struct SbArgs {
+struct __attribute__((aligned(16))) U3 {
+  uint32_t x, y, z;
+};
+
+struct QArgs {
   MatDev m;
   const uint16_t* X;
   void* Y;
@@ -61,363 +67,294 @@ struct SbArgs {
   int out_f32;
 };
 
-// v_perm selector of one weight: digit d (t = d - 1) picks fp16 half d of
-// the source pair {lo: halves 0, 1; hi: half 2}.
-__device__ constexpr uint32_t digit_selector(int d) { return (uint32_t)(2 * d) | ((uint32_t)(2 * d + 1) << 8); }
+// LDS layout (bytes): table, row pointers [R + 1], record flags [R * G],
+// record slots [R * G] x 32 B; after the main loop the partial sums
+// [waves][RT][CT][64 lanes] x 16 B overlay it.
+__host__ __device__ constexpr int q_flag_off(int R) { return kQLutBytes + 4 * (R + 1); }
+__host__ __device__ constexpr int q_rec_off(int R, int G) { return (q_flag_off(R) + R * G + 15) & ~15; }
+__host__ __device__ constexpr int q_stage_bytes(int R, int G) { return q_rec_off(R, G) + 32 * R * G; }
+__host__ __device__ constexpr int q_red_bytes(int RT, int CT) { return kQWaves * RT * CT * 64 * 16; }
 
-__device__ inline float h2f(uint32_t b) { return (float)__builtin_bit_cast(_Float16, (uint16_t)b); }
-__device__ inline uint32_t f2h(float a) { return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)a); }
+__device__ inline uint32_t q_pattern(int t) { return t > 0 ? 0x3C00u : (t < 0 ? 0xBC00u : 0u); }
 
-// Quotient and remainder of i / d for 0 <= i < 2^24, d >= 1 (float estimate,
-// corrected by one step).
-__device__ inline int divide(int i, int d, float inv, int& rem) {
-  int q = (int)((float)i * inv);
-  int r = i - q * d;
-  if (r < 0) { --q; r += d; }
-  if (r >= d) { ++q; r -= d; }
-  rem = r;
-  return q;
+// Table entry of code c: fp16 patterns of (t0, t1), (t2, t3), (t4, 0);
+// codes 243..255 read as zeros.
+__device__ inline uint4 q_entry(int c) {
+  uint32_t t[5];
+  uint32_t d = (uint32_t)c;
+#pragma unroll
+  for (int i = 0; i < 5; ++i) {
+    const uint32_t qd = (d * 171u) >> 9;   // d / 3 for d < 256
+    t[i] = c < 243 ? q_pattern((int)(d - 3u * qd) - 1) : 0u;
+    d = qd;
+  }
+  return uint4{t[0] | (t[1] << 16), t[2] | (t[3] << 16), t[4], 0u};
 }
 
-template <int RT, int KS, int CT>
-__global__ void __launch_bounds__(64 * RT * KS) sb_kernel(SbArgs a) {
-  constexpr int T = 64 * RT * KS;
-  constexpr int R = 16 * RT;
-  constexpr int kPieces = (3 * kMaxPairs + T - 1) / T;     // 8-byte code pieces per thread
-  constexpr int kPairsPerThread = (kMaxPairs + T - 1) / T;
-  constexpr int D = CT == 1 ? 4 : (CT == 2 ? 2 : 1);       // groups per X gather stage
+// LDS byte address of this lane's table copy for byte BY of dword w:
+// bytes [slot, code, 0, 0].
+template <int BY>
+__device__ inline uint32_t q_addr(uint32_t w, uint32_t slot) {
+  return __builtin_amdgcn_perm(slot, w, 0x0C0C0004u | (BY << 8));
+}
 
-  __shared__ uint4 lut[kLutEntries * kLutCopies];
-  extern __shared__ uint4 dyn[];
+// Window u (inputs 8u .. 8u+7 of a group): first code byte, trit phase
+// (index of its first trit in that byte) and last code byte.
+__host__ __device__ constexpr int win_byte(int u) { return (8 * u) / 5; }
+__host__ __device__ constexpr int win_phase(int u) { return (8 * u) % 5; }
+__host__ __device__ constexpr int win_last(int u) { return (8 * u + 7) / 5; }
+
+// Table address of code byte j of a group whose bytes 0..23 are w[0..5] and
+// bytes 24, 25 the low half of w[6] (j is a constant after unrolling).
+__device__ __attribute__((always_inline)) inline uint32_t code_byte_addr(const uint32_t (&w)[7], int j,
+                                                                         uint32_t slot) {
+  const uint32_t word = j < 24 ? w[j >> 2] : w[6];
+  switch (j < 24 ? (j & 3) : j - 24) {
+    case 0: return q_addr<0>(word, slot);
+    case 1: return q_addr<1>(word, slot);
+    case 2: return q_addr<2>(word, slot);
+    default: return q_addr<3>(word, slot);
+  }
+}
+
+// Patterns of a window of phase o from the table entries of its bytes: the
+// window's 8 trits are trits o..4 of e0's byte, then e1's, then e2's.
+__device__ __attribute__((always_inline)) inline void window_patterns(int o, const U3& e0, const U3& e1,
+                                                                      const U3& e2, uint32_t (&d)[4]) {
+  const uint32_t a01 = __builtin_amdgcn_alignbit(e0.y, e0.x, 16), a12 = __builtin_amdgcn_alignbit(e0.z, e0.y, 16);
+  const uint32_t b01 = __builtin_amdgcn_alignbit(e1.y, e1.x, 16), b12 = __builtin_amdgcn_alignbit(e1.z, e1.y, 16);
+  switch (o) {
+    case 0: d[0] = e0.x; d[1] = e0.y; d[2] = e0.z | (e1.x << 16); d[3] = b01; break;
+    case 1: d[0] = a01; d[1] = a12; d[2] = e1.x; d[3] = e1.y; break;
+    case 2: d[0] = e0.y; d[1] = e0.z | (e1.x << 16); d[2] = b01; d[3] = b12; break;
+    case 3: d[0] = a12; d[1] = e1.x; d[2] = e1.y; d[3] = e1.z | (e2.x << 16); break;
+    default: d[0] = e0.z | (e1.x << 16); d[1] = b01; d[2] = b12; d[3] = e2.x; break;
+  }
+}
+
+// p * s + c on two fp16 halves; p and c are fp16 bit pairs (a plain
+// uint32 must never meet a half2v by value conversion).
+__device__ inline uint32_t hfma2(uint32_t p, half2v s, uint32_t c) {
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_fma(__builtin_bit_cast(half2v, p), s,
+                                                                __builtin_bit_cast(half2v, c)));
+}
+
+__device__ inline half2v hsplat(uint32_t h) {
+  const _Float16 v = __builtin_bit_cast(_Float16, (uint16_t)h);
+  return half2v{v, v};
+}
+
+template <int RT, int CT, int QPW>
+__global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  constexpr int R = 16 * RT;
+  constexpr int D = 3;                    // X chunks loaded ahead of use
+  constexpr int NW = QPW * kWindows;      // k-steps of this wave
 
   const MatDev& m = a.m;
   const int G = m.n_groups;
-  const int P = G * R;
-  uint8_t* sbase = reinterpret_cast<uint8_t*>(dyn);
-  uint32_t* w_s = reinterpret_cast<uint32_t*>(sbase);                        // [P][8] plane 0
-  uint32_t* r_s = reinterpret_cast<uint32_t*>(sbase + P * kSlotBytes);       // [P][8] plane 1
-  int* rowptr_s = reinterpret_cast<int*>(sbase + 2 * P * kSlotBytes);        // [R + 1]
-  uint16_t* s0_s = reinterpret_cast<uint16_t*>(rowptr_s + R + 1);            // [P]
-  uint16_t* m0_s = s0_s + P;                                                 // [P] per-group offsets
-  uint8_t* hr_s = reinterpret_cast<uint8_t*>(m0_s + P);                      // [P] record present
-  // Per-group offsets are optional; without them the scales stand in as a
-  // readable address and the staged values are unused.
-  const bool has_off = m.offset0 != nullptr;
-  const uint16_t* off_src = has_off ? m.offset0 : m.scale0;
-
+  const int64_t K = (int64_t)G * kGroup;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
+  const int q = lane >> 4;                // group of the quad (A and B operands)
+  const int r16 = lane & 15;              // A: row of the tile; B: batch column
+  const uint32_t slot = (uint32_t)r16 << 4;
   const int row0 = blockIdx.x * R;
   const int nrows = min(R, m.n_out - row0);
-  const int np = nrows * G;                      // pairs of this workgroup, f - f0 = row * G + g
-  const int64_t f0 = (int64_t)row0 * G;
   const int64_t ngroups = (int64_t)m.n_out * G;
-  const float invG = 1.0f / (float)G;
-  const float inv3G = 1.0f / (float)(3 * G);
+  const bool has_off = m.offset0 != nullptr;
+  const bool has_rec = m.nnz1 > 0;
+
+  unsigned char* lut = lds;
+  int* rowptr_s = reinterpret_cast<int*>(lds + kQLutBytes);
+  uint8_t* flag_s = lds + q_flag_off(R);
+  uint4* rec_s = reinterpret_cast<uint4*>(lds + q_rec_off(R, G));
 
   // ---- 1. Loads, all issued before any wait, every one unconditional at a
-  // clamped (in-bounds) address: a load whose destination is also written on
-  // another path would force a wait for it.  Row pointers first, so the
-  // first LDS writes wait for them alone.
-  int kb = 0, ke = 0, rp = 0;
-  if (m.nnz1 > 0) {
-    kb = m.rowptr1[row0];
-    ke = m.rowptr1[row0 + nrows];
-    rp = m.rowptr1[row0 + min(tid, nrows)];
-  }
-  const uint64_t* mainp = reinterpret_cast<const uint64_t*>(m.codes0 + 24 * f0);
-  const uint16_t* tailp = reinterpret_cast<const uint16_t*>(m.codes0 + 24 * ngroups) + f0;
-  uint64_t pc[kPieces];
-  uint32_t tl[kPairsPerThread], sc[kPairsPerThread], mo[kPairsPerThread];
-#pragma unroll
-  for (int u = 0; u < kPieces; ++u) pc[u] = mainp[min(tid + u * T, 3 * np - 1)];
-#pragma unroll
-  for (int u = 0; u < kPairsPerThread; ++u) {
-    const int i = min(tid + u * T, np - 1);
-    tl[u] = tailp[i];
-    sc[u] = m.scale0[f0 + i];
-    mo[u] = off_src[f0 + i];
-  }
+  // clamped address (a load whose destination is also written on another
+  // path forces an early wait).  Row pointers, the codes and scales of
+  // every (row tile, quad) of this wave, then the first steps' X.
+  const int32_t* rp_src = has_rec ? m.rowptr1 : reinterpret_cast<const int32_t*>(m.codes0);
+  const int32_t kb_l = rp_src[row0];
+  const int32_t ke_l = rp_src[row0 + nrows];
+  const int32_t rp_l = rp_src[row0 + min(tid, nrows)];
+  const uint16_t* off_src = has_off ? m.offset0 : m.scale0;
+  const uint16_t* tail_src = reinterpret_cast<const uint16_t*>(m.codes0 + 24 * ngroups);
 
-  // ---- 2. Selector table (one entry per thread, written to every copy).
-  for (int c = tid; c < kLutEntries; c += T) {
-    uint32_t sel[5];
-    int cc = c;
+  uint32_t cw[QPW][RT][7];   // code bytes 0..23, then bytes 24, 25
+  uint32_t sc[QPW][RT];      // s0 | offset << 16
 #pragma unroll
-    for (int i = 0; i < 5; ++i) {
-      const int q = (cc * 171) >> 9;    // cc / 3 for cc < 256
-      sel[i] = c < 243 ? digit_selector(cc - 3 * q) : 0x0C0Cu;   // invalid codes read as zeros
-      cc = q;
-    }
-    const uint4 e = make_uint4(sel[0] | (sel[1] << 16), sel[2] | (sel[3] << 16), sel[4] | (0x0C0Cu << 16), 0u);
-    // Every copy is identical; the rotation spreads one store instruction's
-    // lanes over the banks.
+  for (int qi = 0; qi < QPW; ++qi) {
+    const int g = min(4 * (wave * QPW + qi) + q, G - 1);
 #pragma unroll
-    for (int k = 0; k < kLutCopies; ++k) lut[c * kLutCopies + ((k + c) & (kLutCopies - 1))] = e;
-  }
-
-  // ---- 3. Plane-0 data to LDS: slot (g, row) = bytes 0..23, tail bytes,
-  // two pad codes 121 (zero trits).
-  if (m.nnz1 > 0 && tid <= nrows) rowptr_s[tid] = rp;
+    for (int rt = 0; rt < RT; ++rt) {
+      const int r = min(16 * rt + r16, nrows - 1);
+      const int64_t f = (int64_t)(row0 + r) * G + g;
+      const uint64_t* mp = reinterpret_cast<const uint64_t*>(m.codes0 + 24 * f);
 #pragma unroll
-  for (int u = 0; u < kPieces; ++u) {
-    const int i = tid + u * T;
-    if (i < 3 * np) {
-      int rem;
-      const int row = divide(i, 3 * G, inv3G, rem);
-      const int g = rem / 3, part = rem - 3 * (rem / 3);
-      uint32_t* d = w_s + 8 * (g * R + row) + 2 * part;
-      d[0] = (uint32_t)pc[u];
-      d[1] = (uint32_t)(pc[u] >> 32);
-    }
-  }
-#pragma unroll
-  for (int u = 0; u < kPairsPerThread; ++u) {
-    const int i = tid + u * T;
-    if (i < np) {
-      int g;
-      const int row = divide(i, G, invG, g);
-      const int p = g * R + row;
-      w_s[8 * p + 6] = tl[u] | 0x79790000u;
-      s0_s[p] = (uint16_t)sc[u];
-      m0_s[p] = (uint16_t)mo[u];
-    }
-  }
-  for (int p = tid; p < P; p += T) hr_s[p] = 0;
-  __syncthreads();
-
-  // ---- 4. Plane-1 records of the workgroup's rows (CSR range kb..ke).
-  if (ke > kb) {
-    const uint64_t* rmain = reinterpret_cast<const uint64_t*>(m.codes1);
-    const uint16_t* rtail = reinterpret_cast<const uint16_t*>(m.codes1 + 24 * m.nnz1);
-    for (int k0 = kb; k0 < ke; k0 += kRecBatch * T) {
-      uint64_t rpc[kRecBatch][3];
-      uint32_t rt[kRecBatch], rm[kRecBatch];
-      int rg[kRecBatch];
-#pragma unroll
-      for (int u = 0; u < kRecBatch; ++u) {
-        const int k = min(k0 + tid + u * T, ke - 1);
-#pragma unroll
-        for (int part = 0; part < 3; ++part) rpc[u][part] = rmain[3 * (int64_t)k + part];
-        rt[u] = rtail[k];
-        rm[u] = (uint32_t)m.offset1[k] | ((uint32_t)m.scale1[k] << 16);
-        rg[u] = (int)m.gidx1[k];
+      for (int i = 0; i < 3; ++i) {
+        const uint64_t v = mp[i];
+        cw[qi][rt][2 * i] = (uint32_t)v;
+        cw[qi][rt][2 * i + 1] = (uint32_t)(v >> 32);
       }
-#pragma unroll
-      for (int u = 0; u < kRecBatch; ++u) {
-        const int k = k0 + tid + u * T;
-        if (k < ke && rg[u] < G) {
-          // Row of record k: the last r with rowptr_s[r] <= k.
-          int lo = 0, hi = nrows;
-          while (hi - lo > 1) {
-            const int mid = (lo + hi) >> 1;
-            if (rowptr_s[mid] <= k) lo = mid; else hi = mid;
-          }
-          const int p = rg[u] * R + lo;
-          uint32_t* d = r_s + 8 * p;
-#pragma unroll
-          for (int part = 0; part < 3; ++part) {
-            d[2 * part] = (uint32_t)rpc[u][part];
-            d[2 * part + 1] = (uint32_t)(rpc[u][part] >> 32);
-          }
-          d[6] = rt[u] | 0x79790000u;
-          d[7] = rm[u];
-          hr_s[p] = 1;
-        }
-      }
+      cw[qi][rt][6] = tail_src[f];
+      sc[qi][rt] = (uint32_t)m.scale0[f] | ((uint32_t)off_src[f] << 16);
     }
   }
-  __syncthreads();
 
-  // ---- 5. Main loop: this wave's row tile over its K range.
-  const int rt = wave % RT;
-  const int ks = wave / RT;
-  const int gper = (G + KS - 1) / KS;
-  const int gb = ks * gper;
-  const int ge = min(G, gb + gper);
-  const int row_l = 16 * rt + (lane & 15);       // A operand row of this lane
-  const int q = lane >> 4;                        // k block of this lane
-  const uint32_t qsh = 8u * q;
-  const int n = lane & 15;                        // B operand batch column
-  const uint32_t xsh = (q & 1) ? 2u : 0u;         // odd code bytes start one half later
-  const int copy = lane & (kLutCopies - 1);
-
-  float4v acc[CT];
-#pragma unroll
-  for (int c = 0; c < CT; ++c) acc[c] = float4v{0.f, 0.f, 0.f, 0.f};
-
-  // Each workgroup walks its K range from a different starting group, so the
-  // workgroups of a chip do not all read the same slice of X at the same
-  // time.  The order is fixed per workgroup, so results stay reproducible.
-  const int nG = ge - gb;
-  const int rot = nG > 0 ? (int)(blockIdx.x % (unsigned)nG) : 0;
-  auto group_at = [&](int t) {   // t-th group visited; past the range: G - 1 (read, never used)
-    if (t >= nG) return G - 1;
-    const int u = t + rot;
-    return gb + (u >= nG ? u - nG : u);
-  };
-
-  // X gathers, in stages of D groups loaded one stage ahead (ping-pong
-  // buffers, so each wait covers exactly the stage being consumed).  Loads
-  // are unconditional: a batch column past B reads row B - 1 (its column of C
-  // is never stored) and a group past the range reads group G - 1.  Byte 25
-  // (inputs 125..127) is loaded from input 122 and realigned when consumed;
-  // pad bytes 26, 27 are zeroed then.
-  typedef uint32_t XStage[D][CT][kStepsPerGroup][3];
-  auto gather = [&](XStage& dst, int t_first) {
-#pragma unroll
-    for (int d = 0; d < D; ++d) {
-      const int g = group_at(t_first + d);
-#pragma unroll
-      for (int c = 0; c < CT; ++c) {
-        const int b = min(16 * c + n, a.B - 1);
-        const uint16_t* xrow = a.X + (int64_t)b * (G * kGroup) + kGroup * g;
-#pragma unroll
-        for (int s = 0; s < kStepsPerGroup; ++s) {
-          const int j = 4 * s + q;                  // code byte of this lane
-          const int off = s < kStepsPerGroup - 1 ? 5 * j - (j & 1) : (q == 1 ? 122 : 120);
-          const uint32_t* p = reinterpret_cast<const uint32_t*>(xrow + off);
-          dst[d][c][s][0] = p[0];
-          dst[d][c][s][1] = p[1];
-          dst[d][c][s][2] = p[2];
-        }
-      }
-    }
-  };
-
-  // Staged weights of one (group, row) pair: plane-0 code words, scale,
-  // record flag and the record slot (read whether or not it is used).
-  struct Slot {
-    uint4 w0, w1, r0, r1;
-    uint32_t s0, m0, hr;
-  };
-  auto read_slot = [&](int g) {
-    const int p = g * R + row_l;
-    Slot v;
-    v.w0 = *reinterpret_cast<const uint4*>(w_s + 8 * p);
-    v.w1 = *reinterpret_cast<const uint4*>(w_s + 8 * p + 4);
-    v.r0 = *reinterpret_cast<const uint4*>(r_s + 8 * p);
-    v.r1 = *reinterpret_cast<const uint4*>(r_s + 8 * p + 4);
-    v.s0 = s0_s[p];
-    v.m0 = m0_s[p];
-    v.hr = hr_s[p];
-    return v;
-  };
-
-  // One group: table reads for all seven k-steps first, then the products.
-  auto consume = [&](const uint32_t (&xg)[CT][kStepsPerGroup][3], const Slot& cur) {
-    u4v xo[CT][kStepsPerGroup];
-#pragma unroll
-    for (int c = 0; c < CT; ++c)
-#pragma unroll
-      for (int s = 0; s < kStepsPerGroup; ++s) {
-        uint32_t l0 = xg[c][s][0], l1 = xg[c][s][1], l2 = xg[c][s][2];
-        if (s == kStepsPerGroup - 1) {
-          if (q == 1) { l0 = l1; l1 = l2; l2 = 0u; }       // inputs 125..127 from 122..127
-          else if (q >= 2) { l0 = 0u; l1 = 0u; l2 = 0u; }  // pad bytes
-        }
-        xo[c][s] = u4v{__builtin_amdgcn_alignbyte(l1, l0, xsh), __builtin_amdgcn_alignbyte(l2, l1, xsh),
-                       (l2 >> (8 * xsh)) & 0xFFFFu, 0u};
-      }
-    const uint32_t sw[kStepsPerGroup] = {cur.w0.x, cur.w0.y, cur.w0.z, cur.w0.w, cur.w1.x, cur.w1.y, cur.w1.z};
-    uint4 e[kStepsPerGroup];
-#pragma unroll
-    for (int s = 0; s < kStepsPerGroup; ++s) e[s] = lut[((sw[s] >> qsh) & 0xFFu) * kLutCopies + copy];
-    // Halves {-s0, +0, +s0}; with per-group offsets {mu0 - s0, mu0, mu0 + s0},
-    // each rounded once from fp32 as in the dense dequantisation.
-    uint32_t lo0 = cur.s0 ^ 0x8000u, hi0 = cur.s0;
-    if (has_off) {
-      const float m0 = 0.0f + h2f(cur.m0), s0 = h2f(cur.s0);
-      lo0 = f2h(m0 - s0) | (f2h(m0) << 16);
-      hi0 = f2h(m0 + s0);
-    }
-    uint32_t av[kStepsPerGroup][3];
-#pragma unroll
-    for (int s = 0; s < kStepsPerGroup; ++s) {
-      av[s][0] = __builtin_amdgcn_perm(hi0, lo0, e[s].x);
-      av[s][1] = __builtin_amdgcn_perm(hi0, lo0, e[s].y);
-      av[s][2] = __builtin_amdgcn_perm(hi0, lo0, e[s].z);
-    }
-    const bool rec = cur.hr != 0;
-    if (__ballot(rec) != 0) {
-      // Plane 1 (lanes without a record add zeros): halves {mu - s1, mu, mu + s1}.
-      const uint32_t ms = cur.r1.w;
-      const float mu = h2f(ms & 0xFFFFu), s1 = h2f(ms >> 16);
-      const uint32_t lo1 = rec ? (f2h(mu - s1) | ((ms & 0xFFFFu) << 16)) : 0u;
-      const uint32_t hi1 = rec ? f2h(mu + s1) : 0u;
-      const uint32_t rw[kStepsPerGroup] = {cur.r0.x, cur.r0.y, cur.r0.z, cur.r0.w, cur.r1.x, cur.r1.y, cur.r1.z};
-      uint4 e1[kStepsPerGroup];
-#pragma unroll
-      for (int s = 0; s < kStepsPerGroup; ++s) e1[s] = lut[((rw[s] >> qsh) & 0xFFu) * kLutCopies + copy];
-#pragma unroll
-      for (int s = 0; s < kStepsPerGroup; ++s) {
-        const uint32_t b1[3] = {__builtin_amdgcn_perm(hi1, lo1, e1[s].x), __builtin_amdgcn_perm(hi1, lo1, e1[s].y),
-                                __builtin_amdgcn_perm(hi1, lo1, e1[s].z)};
-#pragma unroll
-        for (int i = 0; i < 3; ++i)
-          av[s][i] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, av[s][i]) + __builtin_bit_cast(half2v, b1[i]));
-      }
-    }
-#pragma unroll
-    for (int s = 0; s < kStepsPerGroup; ++s) {
-      const half8 A = __builtin_bit_cast(half8, u4v{av[s][0], av[s][1], av[s][2], 0u});
-#pragma unroll
-      for (int c = 0; c < CT; ++c)
-        acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, __builtin_bit_cast(half8, xo[c][s]), acc[c], 0, 0, 0);
-    }
-  };
-
-  XStage xa, xb;
-  gather(xa, 0);
-  Slot cur = read_slot(group_at(0));
-  auto run_stage = [&](const XStage& xs, int t_first) {
-#pragma unroll
-    for (int d = 0; d < D; ++d) {
-      const int t = t_first + d;
-      const Slot nxt = read_slot(group_at(t + 1));   // next group's slot, read one group ahead
-      if (t < nG) consume(xs[d], cur);
-      cur = nxt;
-    }
-  };
-  for (int t0 = 0; t0 < nG; t0 += 2 * D) {
-    gather(xb, t0 + D);
-    run_stage(xa, t0);
-    gather(xa, t0 + 2 * D);
-    run_stage(xb, t0 + D);
-  }
-
-  // ---- 6. K-split partial sums, added in a fixed order, then Y.
-  if constexpr (KS > 1) {
-    __syncthreads();                              // staging buffers are free now
-    float4v* red = reinterpret_cast<float4v*>(sbase);
-    if (ks > 0) {
-#pragma unroll
-      for (int c = 0; c < CT; ++c) red[(((rt * (KS - 1)) + ks - 1) * CT + c) * 64 + lane] = acc[c];
-    }
-    __syncthreads();
-    if (ks == 0) {
-#pragma unroll
-      for (int k2 = 1; k2 < KS; ++k2)
-#pragma unroll
-        for (int c = 0; c < CT; ++c) acc[c] += red[(((rt * (KS - 1)) + k2 - 1) * CT + c) * 64 + lane];
-    }
-  }
-  if (ks == 0) {
+  u4v xb[D + 1][CT];
+  auto issue_x = [&](int F) {   // k-step F of this wave: quad F / 16, window F % 16
+    const int qi = F / kWindows, u = F % kWindows;
+    const int g = min(4 * (wave * QPW + qi) + q, G - 1);
 #pragma unroll
     for (int c = 0; c < CT; ++c) {
-      const int b = 16 * c + n;
-      if (b < a.B) {
+      const int b = min(16 * c + r16, a.B - 1);
+      xb[F % (D + 1)][c] = *reinterpret_cast<const u4v*>(a.X + (int64_t)b * K + kGroup * g + 8 * u);
+    }
+  };
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int r = 16 * rt + 4 * q + i;
-          if (r < nrows) {
-            const int64_t o = (int64_t)b * m.n_out + row0 + r;
-            if (a.out_f32)
-              reinterpret_cast<float*>(a.Y)[o] = acc[c][i];
-            else
-              reinterpret_cast<uint16_t*>(a.Y)[o] = (uint16_t)f2h(acc[c][i]);
-          }
+  for (int F = 0; F < D; ++F)
+    if (F < NW) issue_x(F);
+
+  // ---- 2. Table (one code and half of its copies per thread; at step k
+  // the copy index is rotated by the code so one store instruction's lanes
+  // spread over the banks), record flags cleared, row pointers.
+  for (int t = tid; t < 512; t += kQThreads) {
+    const int c = t & 255, h = t >> 8;
+    const uint4 e = q_entry(c);
+#pragma unroll
+    for (int k = 0; k < kQRep / 2; ++k)
+      reinterpret_cast<uint4*>(lut)[c * kQRep + ((8 * h + k + c) & (kQRep - 1))] = e;
+  }
+  for (int i = tid; i < (q_rec_off(R, G) - q_flag_off(R)) / 4; i += kQThreads)
+    reinterpret_cast<uint32_t*>(flag_s)[i] = 0u;
+  if (tid <= nrows) rowptr_s[tid] = rp_l;
+  __syncthreads();
+
+  // ---- 3. Plane-1 records of the workgroup's rows (CSR range kb..ke) to
+  // their (row, group) slots.
+  const int kb = has_rec ? kb_l : 0, ke = has_rec ? ke_l : 0;
+  for (int k0 = kb; k0 < ke; k0 += kQThreads) {
+    const int k = k0 + tid;
+    if (k < ke) {
+      const uint64_t* rm = reinterpret_cast<const uint64_t*>(m.codes1) + 3 * (int64_t)k;
+      const uint64_t v0 = rm[0], v1 = rm[1], v2 = rm[2];
+      const uint32_t tl = reinterpret_cast<const uint16_t*>(m.codes1 + 24 * m.nnz1)[k];
+      const uint32_t ms = (uint32_t)m.offset1[k] | ((uint32_t)m.scale1[k] << 16);
+      const int gg = (int)m.gidx1[k];
+      // Row of record k: the last r with rowptr_s[r] <= k.
+      int lo = 0, hi = nrows;
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (rowptr_s[mid] <= k) lo = mid; else hi = mid;
+      }
+      if (gg < G) {
+        const int p = lo * G + gg;
+        rec_s[2 * p] = uint4{(uint32_t)v0, (uint32_t)(v0 >> 32), (uint32_t)v1, (uint32_t)(v1 >> 32)};
+        rec_s[2 * p + 1] = uint4{(uint32_t)v2, (uint32_t)(v2 >> 32), tl, ms};
+        flag_s[p] = 1;
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- 4. Main loop: quads of this wave, 16 k-steps each, all row tiles
+  // and batch column tiles.
+  float4v acc[RT][CT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int c = 0; c < CT; ++c) acc[rt][c] = float4v{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+  for (int qi = 0; qi < QPW; ++qi) {
+    const int g = 4 * (wave * QPW + qi) + q;
+    // Per row tile: weight = p0 * s0 + c0 (+ p1 * s1 with a record), c0 =
+    // group offset + record offset (each zero where absent); lanes past the
+    // rows or groups get zero weights.
+    half2v s0v[RT], s1v[RT];
+    uint32_t c0v[RT];
+    bool hr[RT];
+    uint32_t rc[RT][7];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int r = 16 * rt + r16;
+      const bool valid = g < G && r < nrows;
+      const int p = min(r, nrows - 1) * G + min(g, G - 1);
+      const uint4 ra = rec_s[2 * p], rb = rec_s[2 * p + 1];
+      hr[rt] = valid && flag_s[p] != 0;
+      const float mu = hr[rt] ? h2f(rb.w & 0xFFFFu) : 0.0f;
+      const uint32_t s1b = hr[rt] ? (rb.w >> 16) : 0u;
+      const float m0 = has_off ? h2f(sc[qi][rt] >> 16) : 0.0f;
+      s0v[rt] = hsplat(valid ? (sc[qi][rt] & 0xFFFFu) : 0u);
+      const uint32_t c0 = valid ? f2h(m0 + mu) : 0u;
+      c0v[rt] = c0 | (c0 << 16);
+      s1v[rt] = hsplat(s1b);
+      rc[rt][0] = ra.x; rc[rt][1] = ra.y; rc[rt][2] = ra.z; rc[rt][3] = ra.w;
+      rc[rt][4] = rb.x; rc[rt][5] = rb.y; rc[rt][6] = rb.z;
+    }
+
+    U3 e0[RT][kGroupBytes], e1[RT][kGroupBytes];   // table entries, read at first use
+#pragma unroll
+    for (int u = 0; u < kWindows; ++u) {
+      const int F = qi * kWindows + u;
+      if (F + D < NW) issue_x(F + D);
+      const u4v (&xv)[CT] = xb[F % (D + 1)];
+      const int j0 = win_byte(u), jl = win_last(u), jn = u == 0 ? 0 : win_last(u - 1) + 1;
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+        for (int k = 0; k < 3; ++k)   // the window's bytes not read by the previous one
+          if (jn + k <= jl) e0[rt][jn + k] = *reinterpret_cast<const U3*>(lut + code_byte_addr(cw[qi][rt], jn + k, slot));
+        uint32_t p[4], w[4];
+        window_patterns(win_phase(u), e0[rt][j0], e0[rt][j0 + 1], e0[rt][jl], p);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) w[i] = hfma2(p[i], s0v[rt], c0v[rt]);
+        if (hr[rt]) {
+#pragma unroll
+          for (int k = 0; k < 3; ++k)
+            if (jn + k <= jl) e1[rt][jn + k] = *reinterpret_cast<const U3*>(lut + code_byte_addr(rc[rt], jn + k, slot));
+          uint32_t p1[4];
+          window_patterns(win_phase(u), e1[rt][j0], e1[rt][j0 + 1], e1[rt][jl], p1);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) w[i] = hfma2(p1[i], s1v[rt], w[i]);
+        }
+        const half8 A = __builtin_bit_cast(half8, u4v{w[0], w[1], w[2], w[3]});
+#pragma unroll
+        for (int c = 0; c < CT; ++c)
+          acc[rt][c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, __builtin_bit_cast(half8, xv[c]), acc[rt][c], 0, 0, 0);
+      }
+    }
+  }
+
+  // ---- 5. Partial sums of the waves, added in wave order, then Y.
+  __syncthreads();   // every wave is done with the table and the records
+  float4v* red = reinterpret_cast<float4v*>(lds);
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int c = 0; c < CT; ++c) red[((wave * RT + rt) * CT + c) * 64 + lane] = acc[rt][c];
+  __syncthreads();
+  constexpr int kItems = RT * CT * 64;
+  for (int it = tid; it < kItems; it += kQThreads) {
+    // Four consecutive threads hold 16 consecutive rows of one column.
+    const int qq = it & 3, n = (it >> 2) & 15, c = (it >> 6) % CT, rt = (it >> 6) / CT;
+    const int ln = 16 * qq + n;
+    float4v s = red[(rt * CT + c) * 64 + ln];
+#pragma unroll
+    for (int w = 1; w < kQWaves; ++w) s += red[((w * RT + rt) * CT + c) * 64 + ln];
+    const int b = 16 * c + n;
+    if (b < a.B) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 16 * rt + 4 * qq + i;
+        if (r < nrows) {
+          const int64_t o = (int64_t)b * m.n_out + row0 + r;
+          if (a.out_f32)
+            reinterpret_cast<float*>(a.Y)[o] = s[i];
+          else
+            reinterpret_cast<uint16_t*>(a.Y)[o] = (uint16_t)f2h(s[i]);
         }
       }
     }
@@ -437,11 +374,6 @@ constexpr int kRows = 16 * kWaves;      // W rows per workgroup
 constexpr int kSlots = 160;             // k slots per 128-wide step
 constexpr int kStride = 168;            // LDS row stride in halves
 constexpr int kMaxColTiles = TQ_MAX_BATCH / 16;
-
-
-__device__ inline uint32_t trit_pattern(int t) {
-  return t > 0 ? 0x3C00u : (t < 0 ? 0xBC00u : 0u);
-}
 
 
 __device__ inline int64_t byte_offset(int64_t f, int j, int64_t n) {
@@ -474,9 +406,9 @@ __global__ void __launch_bounds__(kThreads) fallback_kernel(MatDev m, const uint
         t[i] = cc % 3 - 1;
         cc /= 3;
       }
-      v.x = trit_pattern(t[0]) | (trit_pattern(t[1]) << 16);
-      v.y = trit_pattern(t[2]) | (trit_pattern(t[3]) << 16);
-      v.z = trit_pattern(t[4]);
+      v.x = q_pattern(t[0]) | (q_pattern(t[1]) << 16);
+      v.y = q_pattern(t[2]) | (q_pattern(t[3]) << 16);
+      v.z = q_pattern(t[4]);
     }
     lut[c] = v;
   }
@@ -597,24 +529,44 @@ __global__ void __launch_bounds__(kThreads) fallback_kernel(MatDev m, const uint
 }
 
 
-typedef void (*SbKernel)(SbArgs);
 
-SbKernel sb_select(int RT, int ci) {
-  static const SbKernel table[4][3] = {
-      {sb_kernel<1, 4, 1>, sb_kernel<1, 4, 2>, sb_kernel<1, 4, 4>},
-      {sb_kernel<2, 2, 1>, sb_kernel<2, 2, 2>, sb_kernel<2, 2, 4>},
-      {sb_kernel<3, 1, 1>, sb_kernel<3, 1, 2>, sb_kernel<3, 1, 4>},
-      {sb_kernel<4, 1, 1>, sb_kernel<4, 1, 2>, sb_kernel<4, 1, 4>},
-  };
-  return table[RT - 1][ci];
+
+typedef void (*QKernel)(QArgs);
+
+template <int RT, int QPW>
+QKernel q_pick(int CT) {
+  switch (CT) {
+    case 1: return quad_kernel<RT, 1, QPW>;
+    case 2: return quad_kernel<RT, 2, QPW>;
+    case 3: return quad_kernel<RT, 3, QPW>;
+    default:
+      if constexpr (RT == 4) return nullptr;   // not launched: it would spill registers
+      else return quad_kernel<RT, 4, QPW>;
+  }
 }
 
-struct SbDeviceInfo {
-  bool attr_set[4][3] = {};
+// (RT, QPW) pairs with RT * QPW <= kQMaxUnits.
+QKernel q_select(int RT, int QPW, int CT) {
+  switch (RT) {
+    case 1:
+      switch (QPW) {
+        case 1: return q_pick<1, 1>(CT);
+        case 2: return q_pick<1, 2>(CT);
+        case 3: return q_pick<1, 3>(CT);
+        default: return q_pick<1, 4>(CT);
+      }
+    case 2: return QPW == 1 ? q_pick<2, 1>(CT) : q_pick<2, 2>(CT);
+    case 3: return q_pick<3, 1>(CT);
+    default: return q_pick<4, 1>(CT);
+  }
+}
+
+struct QDeviceInfo {
+  bool attr_set[4][4][4] = {};
 };
 
-SbDeviceInfo& sb_device_info() {
-  static thread_local SbDeviceInfo info[64];
+QDeviceInfo& q_device_info() {
+  static thread_local QDeviceInfo info[64];
   int dev = 0;
   (void)hipGetDevice(&dev);
   return info[dev & 63];
@@ -625,34 +577,38 @@ SbDeviceInfo& sb_device_info() {
 hipError_t launch_gemm_smallbatch(const MatDev& m, const uint16_t* X, int B, void* Y, bool out_f32,
                                   hipStream_t s) {
   const int G = m.n_groups;
+  const int NQ = (G + 3) / 4;
+  const int QPW = (NQ + kQWaves - 1) / kQWaves;
   // Rows per workgroup: about one workgroup per CU (256), at most 4 row
-  // tiles, and a staging that fits.
+  // tiles, and at most kQMaxUnits (row tile, quad) units per wave and
+  // kQMaxPairs record slots.
   int RT = (m.n_out + 16 * 256 - 1) / (16 * 256);
   RT = RT < 1 ? 1 : (RT > 4 ? 4 : RT);
-  while (RT > 1 && G * 16 * RT > kMaxPairs) --RT;
-  if (G * 16 * RT > kMaxPairs) {
+  const int CT = (B + 15) / 16;
+  // Four row tiles with four column tiles would spill registers.
+  if (RT == 4 && CT == 4) RT = 3;
+  while (RT > 1 && (RT * QPW > kQMaxUnits || 16 * RT * G > kQMaxPairs)) --RT;
+  if (RT * QPW > kQMaxUnits || 16 * RT * G > kQMaxPairs) {
     const int wgs = (m.n_out + kRows - 1) / kRows;
     hipLaunchKernelGGL(fallback_kernel, dim3(wgs), dim3(kThreads), 0, s, m, X, B, Y, out_f32 ? 1 : 0);
     return hipGetLastError();
   }
-  const int KS = RT == 1 ? 4 : (RT == 2 ? 2 : 1);
-  const int ci = B <= 16 ? 0 : (B <= 32 ? 1 : 2);
-  const int CT = 1 << ci;
   const int R = 16 * RT;
-  const int staged = staged_bytes(G * R, R);
-  const int red = RT * (KS - 1) * CT * 64 * 16;
+  const int staged = q_stage_bytes(R, G);
+  const int red = q_red_bytes(RT, CT);
   const int dyn = staged > red ? staged : red;
-  const SbKernel kern = sb_select(RT, ci);
-  SbDeviceInfo& di = sb_device_info();
-  if (!di.attr_set[RT - 1][ci]) {
+  const QKernel kern = q_select(RT, QPW, CT);
+  if (kern == nullptr) return hipErrorInvalidValue;
+  QDeviceInfo& di = q_device_info();
+  if (!di.attr_set[RT - 1][QPW - 1][CT - 1]) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, kLdsLimit - kLutBytes);
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, kLdsLimit);
     if (e != hipSuccess) return e;
-    di.attr_set[RT - 1][ci] = true;
+    di.attr_set[RT - 1][QPW - 1][CT - 1] = true;
   }
-  SbArgs args{m, X, Y, B, out_f32 ? 1 : 0};
+  QArgs args{m, X, Y, B, out_f32 ? 1 : 0};
   const int wgs = (m.n_out + R - 1) / R;
-  hipLaunchKernelGGL(kern, dim3(wgs), dim3(64 * RT * KS), dyn, s, args);
+  hipLaunchKernelGGL(kern, dim3(wgs), dim3(kQThreads), dyn, s, args);
   return hipGetLastError();
 }
 
