@@ -105,9 +105,9 @@ __host__ __device__ constexpr int win_phase(int u) { return (8 * u) % 5; }
 __host__ __device__ constexpr int win_last(int u) { return (8 * u + 7) / 5; }
 
 // Table address of code byte j of a group whose bytes 0..23 are w[0..5] and
-// bytes 24, 25 the low half of w[6] (j is a constant after unrolling).
-__device__ __attribute__((always_inline)) inline uint32_t code_byte_addr(const uint32_t (&w)[7], int j,
-                                                                         uint32_t slot) {
+// bytes 24, 25 the low half of w[6] (j is a constant after unrolling; w is
+// registers or a record slot in LDS).
+__device__ __attribute__((always_inline)) inline uint32_t code_byte_addr(const uint32_t* w, int j, uint32_t slot) {
   const uint32_t word = j < 24 ? w[j >> 2] : w[6];
   switch (j < 24 ? (j & 3) : j - 24) {
     case 0: return q_addr<0>(word, slot);
@@ -144,11 +144,54 @@ __device__ inline half2v hsplat(uint32_t h) {
   return half2v{v, v};
 }
 
+// Workgroup barrier for LDS data only: waits for this wave's LDS accesses
+// but leaves its global loads in flight (a plain __syncthreads waits for
+// those too).
+__device__ inline void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// One plane-1 record as loaded: code bytes 0..23, bytes 24, 25, mu | s1 << 16, group.
+struct RecLoad {
+  uint64_t v0, v1, v2;
+  uint32_t tl, ms;
+  int gg;
+};
+
+// Record k; a matrix without records reads its plane-0 arrays at k = 0
+// instead (no branch around the loads, whose results are then unused).
+__device__ inline RecLoad load_record(const MatDev& m, int64_t k) {
+  const bool has = m.nnz1 > 0;
+  const uint8_t* codes = has ? m.codes1 : m.codes0;
+  const int64_t n = has ? m.nnz1 : (int64_t)m.n_out * m.n_groups;
+  const uint16_t* mu = has ? m.offset1 : m.scale0;
+  const uint16_t* s1 = has ? m.scale1 : m.scale0;
+  const uint16_t* gi = has ? m.gidx1 : m.scale0;
+  k = has ? k : 0;
+  const uint64_t* rm = reinterpret_cast<const uint64_t*>(codes) + 3 * k;
+  RecLoad r;
+  r.v0 = rm[0];
+  r.v1 = rm[1];
+  r.v2 = rm[2];
+  r.tl = reinterpret_cast<const uint16_t*>(codes + 24 * n)[k];
+  r.ms = (uint32_t)mu[k] | ((uint32_t)s1[k] << 16);
+  r.gg = (int)gi[k];
+  return r;
+}
+
 template <int RT, int CT, int QPW>
 __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   constexpr int R = 16 * RT;
-  constexpr int D = 3;                    // X chunks loaded ahead of use
+  // X is loaded in bursts of L consecutive chunks per lane (a whole
+  // 128-byte line, or half of one when four column tiles leave too few
+  // registers), one burst ahead of use: every line is fetched once and used
+  // whole.  Single 16-byte chunks per step made each line be refetched for
+  // every chunk: the 16 batch rows of a step lie a power-of-two stride apart
+  // and evict each other from L1.
+  constexpr int L = CT <= 2 ? 8 : 4;
   constexpr int NW = QPW * kWindows;      // k-steps of this wave
 
   const MatDev& m = a.m;
@@ -176,9 +219,9 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
   // path forces an early wait).  Row pointers, the codes and scales of
   // every (row tile, quad) of this wave, then the first steps' X.
   const int32_t* rp_src = has_rec ? m.rowptr1 : reinterpret_cast<const int32_t*>(m.codes0);
+  const int32_t rp_l = rp_src[row0 + min(tid, nrows)];
   const int32_t kb_l = rp_src[row0];
   const int32_t ke_l = rp_src[row0 + nrows];
-  const int32_t rp_l = rp_src[row0 + min(tid, nrows)];
   const uint16_t* off_src = has_off ? m.offset0 : m.scale0;
   const uint16_t* tail_src = reinterpret_cast<const uint16_t*>(m.codes0 + 24 * ngroups);
 
@@ -203,19 +246,27 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
     }
   }
 
-  u4v xb[D + 1][CT];
-  auto issue_x = [&](int F) {   // k-step F of this wave: quad F / 16, window F % 16
-    const int qi = F / kWindows, u = F % kWindows;
-    const int g = min(4 * (wave * QPW + qi) + q, G - 1);
+  u4v xb[2][L][CT];
+  auto issue_x = [&](int v) {   // burst v: k-steps v L .. v L + L - 1 of this wave
 #pragma unroll
-    for (int c = 0; c < CT; ++c) {
-      const int b = min(16 * c + r16, a.B - 1);
-      xb[F % (D + 1)][c] = *reinterpret_cast<const u4v*>(a.X + (int64_t)b * K + kGroup * g + 8 * u);
+    for (int k = 0; k < L; ++k) {
+      const int F = v * L + k;
+      const int qi = F / kWindows, u = F % kWindows;
+      const int g = min(4 * (wave * QPW + qi) + q, G - 1);
+#pragma unroll
+      for (int c = 0; c < CT; ++c) {
+        const int b = min(16 * c + r16, a.B - 1);
+        xb[v & 1][k][c] = *reinterpret_cast<const u4v*>(a.X + (int64_t)b * K + kGroup * g + 8 * u);
+      }
     }
   };
-#pragma unroll
-  for (int F = 0; F < D; ++F)
-    if (F < NW) issue_x(F);
+  issue_x(0);
+
+  // The workgroup's first kQThreads plane-1 records, one per thread (a
+  // clamped in-range index where there are fewer; only threads below the
+  // count use theirs).
+  const int kb = has_rec ? kb_l : 0, ke = has_rec ? ke_l : 0;
+  const RecLoad rec0 = load_record(m, min(kb + tid, max(ke - 1, 0)));
 
   // ---- 2. Table (one code and half of its copies per thread; at step k
   // the copy index is rotated by the code so one store instruction's lanes
@@ -230,34 +281,27 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
   for (int i = tid; i < (q_rec_off(R, G) - q_flag_off(R)) / 4; i += kQThreads)
     reinterpret_cast<uint32_t*>(flag_s)[i] = 0u;
   if (tid <= nrows) rowptr_s[tid] = rp_l;
-  __syncthreads();
+  lds_barrier();
 
   // ---- 3. Plane-1 records of the workgroup's rows (CSR range kb..ke) to
   // their (row, group) slots.
-  const int kb = has_rec ? kb_l : 0, ke = has_rec ? ke_l : 0;
-  for (int k0 = kb; k0 < ke; k0 += kQThreads) {
-    const int k = k0 + tid;
-    if (k < ke) {
-      const uint64_t* rm = reinterpret_cast<const uint64_t*>(m.codes1) + 3 * (int64_t)k;
-      const uint64_t v0 = rm[0], v1 = rm[1], v2 = rm[2];
-      const uint32_t tl = reinterpret_cast<const uint16_t*>(m.codes1 + 24 * m.nnz1)[k];
-      const uint32_t ms = (uint32_t)m.offset1[k] | ((uint32_t)m.scale1[k] << 16);
-      const int gg = (int)m.gidx1[k];
-      // Row of record k: the last r with rowptr_s[r] <= k.
-      int lo = 0, hi = nrows;
-      while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (rowptr_s[mid] <= k) lo = mid; else hi = mid;
-      }
-      if (gg < G) {
-        const int p = lo * G + gg;
-        rec_s[2 * p] = uint4{(uint32_t)v0, (uint32_t)(v0 >> 32), (uint32_t)v1, (uint32_t)(v1 >> 32)};
-        rec_s[2 * p + 1] = uint4{(uint32_t)v2, (uint32_t)(v2 >> 32), tl, ms};
-        flag_s[p] = 1;
-      }
+  auto stage = [&](int k, const RecLoad& r) {
+    // Row of record k: the last r with rowptr_s[r] <= k.
+    int lo = 0, hi = nrows;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (rowptr_s[mid] <= k) lo = mid; else hi = mid;
     }
-  }
-  __syncthreads();
+    if (r.gg < G) {
+      const int p = lo * G + r.gg;
+      rec_s[2 * p] = uint4{(uint32_t)r.v0, (uint32_t)(r.v0 >> 32), (uint32_t)r.v1, (uint32_t)(r.v1 >> 32)};
+      rec_s[2 * p + 1] = uint4{(uint32_t)r.v2, (uint32_t)(r.v2 >> 32), r.tl, r.ms};
+      flag_s[p] = 1;
+    }
+  };
+  if (kb + tid < ke) stage(kb + tid, rec0);
+  for (int k = kb + kQThreads + tid; k < ke; k += kQThreads) stage(k, load_record(m, k));
+  lds_barrier();
 
   // ---- 4. Main loop: quads of this wave, 16 k-steps each, all row tiles
   // and batch column tiles.
@@ -276,13 +320,17 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
     half2v s0v[RT], s1v[RT];
     uint32_t c0v[RT];
     bool hr[RT];
-    uint32_t rc[RT][7];
+    // Record codes: in registers where they fit (few column and row tiles),
+    // else read from the LDS slot when used.
+    constexpr bool kRcRegs = CT == 1 || (CT == 2 && RT <= 3);
+    uint32_t rcr[RT][kRcRegs ? 7 : 1];
+    const uint32_t* rcs[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       const int r = 16 * rt + r16;
       const bool valid = g < G && r < nrows;
       const int p = min(r, nrows - 1) * G + min(g, G - 1);
-      const uint4 ra = rec_s[2 * p], rb = rec_s[2 * p + 1];
+      const uint4 rb = rec_s[2 * p + 1];
       hr[rt] = valid && flag_s[p] != 0;
       const float mu = hr[rt] ? h2f(rb.w & 0xFFFFu) : 0.0f;
       const uint32_t s1b = hr[rt] ? (rb.w >> 16) : 0u;
@@ -291,32 +339,43 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
       const uint32_t c0 = valid ? f2h(m0 + mu) : 0u;
       c0v[rt] = c0 | (c0 << 16);
       s1v[rt] = hsplat(s1b);
-      rc[rt][0] = ra.x; rc[rt][1] = ra.y; rc[rt][2] = ra.z; rc[rt][3] = ra.w;
-      rc[rt][4] = rb.x; rc[rt][5] = rb.y; rc[rt][6] = rb.z;
+      rcs[rt] = reinterpret_cast<const uint32_t*>(rec_s + 2 * p);
+      if constexpr (kRcRegs) {
+        const uint4 ra = rec_s[2 * p];
+        rcr[rt][0] = ra.x; rcr[rt][1] = ra.y; rcr[rt][2] = ra.z; rcr[rt][3] = ra.w;
+        rcr[rt][4] = rb.x; rcr[rt][5] = rb.y; rcr[rt][6] = rb.z;
+      }
     }
 
-    U3 e0[RT][kGroupBytes], e1[RT][kGroupBytes];   // table entries, read at first use
+    U3 ep0[RT], ep1[RT];   // table entry of the previous window's last byte (planes 0, 1)
 #pragma unroll
-    for (int u = 0; u < kWindows; ++u) {
-      const int F = qi * kWindows + u;
-      if (F + D < NW) issue_x(F + D);
-      const u4v (&xv)[CT] = xb[F % (D + 1)];
-      const int j0 = win_byte(u), jl = win_last(u), jn = u == 0 ? 0 : win_last(u - 1) + 1;
+    for (int v = 0; v < kWindows / L; ++v) {
+    const int F0 = qi * kWindows + v * L;
+    if (F0 + L < NW) issue_x(F0 / L + 1);
+#pragma unroll
+    for (int k = 0; k < L; ++k) {
+      const int u = v * L + k, F = F0 + k;
+      const u4v (&xv)[CT] = xb[(F / L) & 1][k];
+      const int j0 = win_byte(u), jl = win_last(u);
+      const bool shared = u > 0 && win_last(u - 1) == j0;   // first byte already read
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
-#pragma unroll
-        for (int k = 0; k < 3; ++k)   // the window's bytes not read by the previous one
-          if (jn + k <= jl) e0[rt][jn + k] = *reinterpret_cast<const U3*>(lut + code_byte_addr(cw[qi][rt], jn + k, slot));
+        const U3 a0 = shared ? ep0[rt] : *reinterpret_cast<const U3*>(lut + code_byte_addr(cw[qi][rt], j0, slot));
+        const U3 a1 = *reinterpret_cast<const U3*>(lut + code_byte_addr(cw[qi][rt], j0 + 1, slot));
+        const U3 a2 = jl > j0 + 1 ? *reinterpret_cast<const U3*>(lut + code_byte_addr(cw[qi][rt], jl, slot)) : a1;
+        ep0[rt] = a2;
         uint32_t p[4], w[4];
-        window_patterns(win_phase(u), e0[rt][j0], e0[rt][j0 + 1], e0[rt][jl], p);
+        window_patterns(win_phase(u), a0, a1, a2, p);
 #pragma unroll
         for (int i = 0; i < 4; ++i) w[i] = hfma2(p[i], s0v[rt], c0v[rt]);
         if (hr[rt]) {
-#pragma unroll
-          for (int k = 0; k < 3; ++k)
-            if (jn + k <= jl) e1[rt][jn + k] = *reinterpret_cast<const U3*>(lut + code_byte_addr(rc[rt], jn + k, slot));
+          const uint32_t* rc = kRcRegs ? rcr[rt] : rcs[rt];
+          const U3 b0 = shared ? ep1[rt] : *reinterpret_cast<const U3*>(lut + code_byte_addr(rc, j0, slot));
+          const U3 b1 = *reinterpret_cast<const U3*>(lut + code_byte_addr(rc, j0 + 1, slot));
+          const U3 b2 = jl > j0 + 1 ? *reinterpret_cast<const U3*>(lut + code_byte_addr(rc, jl, slot)) : b1;
+          ep1[rt] = b2;
           uint32_t p1[4];
-          window_patterns(win_phase(u), e1[rt][j0], e1[rt][j0 + 1], e1[rt][jl], p1);
+          window_patterns(win_phase(u), b0, b1, b2, p1);
 #pragma unroll
           for (int i = 0; i < 4; ++i) w[i] = hfma2(p1[i], s1v[rt], w[i]);
         }
@@ -326,16 +385,17 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
           acc[rt][c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, __builtin_bit_cast(half8, xv[c]), acc[rt][c], 0, 0, 0);
       }
     }
+    }
   }
 
   // ---- 5. Partial sums of the waves, added in wave order, then Y.
-  __syncthreads();   // every wave is done with the table and the records
+  lds_barrier();   // every wave is done with the table and the records
   float4v* red = reinterpret_cast<float4v*>(lds);
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int c = 0; c < CT; ++c) red[((wave * RT + rt) * CT + c) * 64 + lane] = acc[rt][c];
-  __syncthreads();
+  lds_barrier();
   constexpr int kItems = RT * CT * 64;
   for (int it = tid; it < kItems; it += kQThreads) {
     // Four consecutive threads hold 16 consecutive rows of one column.
