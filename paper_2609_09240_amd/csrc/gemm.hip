@@ -67,10 +67,11 @@ struct QArgs {
   int out_f32;
 };
 
-// LDS layout (bytes): table, row pointers [R + 1], record flags [R * G],
-// record slots [R * G] x 32 B; after the main loop the partial sums
-// [waves][RT][CT][64 lanes] x 16 B overlay it.
-__host__ __device__ constexpr int q_flag_off(int R) { return kQLutBytes + 4 * (R + 1); }
+// LDS: the table (static, at address 0, so a lane's table address needs no
+// base), then the dynamic part: row pointers [R + 1], record flags
+// [R * G], record slots [R * G] x 32 B (byte offsets below); after the main
+// loop the partial sums [waves][RT][CT][64 lanes] x 16 B overlay it.
+__host__ __device__ constexpr int q_flag_off(int R) { return 4 * (R + 1); }
 __host__ __device__ constexpr int q_rec_off(int R, int G) { return (q_flag_off(R) + R * G + 15) & ~15; }
 __host__ __device__ constexpr int q_stage_bytes(int R, int G) { return q_rec_off(R, G) + 32 * R * G; }
 __host__ __device__ constexpr int q_red_bytes(int RT, int CT) { return kQWaves * RT * CT * 64 * 16; }
@@ -183,6 +184,7 @@ __device__ inline RecLoad load_record(const MatDev& m, int64_t k) {
 
 template <int RT, int CT, int QPW>
 __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
+  __shared__ __attribute__((aligned(16))) unsigned char lut[kQLutBytes];
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   constexpr int R = 16 * RT;
   // X is loaded in bursts of L consecutive chunks per lane (a whole
@@ -209,8 +211,7 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
   const bool has_off = m.offset0 != nullptr;
   const bool has_rec = m.nnz1 > 0;
 
-  unsigned char* lut = lds;
-  int* rowptr_s = reinterpret_cast<int*>(lds + kQLutBytes);
+  int* rowptr_s = reinterpret_cast<int*>(lds);
   uint8_t* flag_s = lds + q_flag_off(R);
   uint4* rec_s = reinterpret_cast<uint4*>(lds + q_rec_off(R, G));
 
@@ -662,7 +663,7 @@ hipError_t launch_gemm_smallbatch(const MatDev& m, const uint16_t* X, int B, voi
   QDeviceInfo& di = q_device_info();
   if (!di.attr_set[RT - 1][QPW - 1][CT - 1]) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, kLdsLimit);
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, kLdsLimit - kQLutBytes);
     if (e != hipSuccess) return e;
     di.attr_set[RT - 1][QPW - 1][CT - 1] = true;
   }
