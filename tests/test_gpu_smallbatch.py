@@ -1,5 +1,7 @@
-"""GPU parity of tq_gemm_smallbatch (LDS-decoded tiles + MFMA) against the
-fp64 oracle, per (batch row, output) within the same bound as the GEMV."""
+"""GPU parity of tq_gemm_smallbatch (B = 1: the GEMV; 2..4: the GEMV's decode
+per batch row; larger: the MFMA kernel over quads of groups, or the
+per-group fallback) against the fp64 oracle, per (batch row, output) within
+the same bound as the GEMV."""
 
 import numpy as np
 import pytest
@@ -61,10 +63,13 @@ def test_deterministic():
 
 @pytest.mark.parametrize("B", [3, 16, 40, 64])
 @pytest.mark.parametrize("n_out,n_in,f2", [
-    (5000, 512, 0.1),      # two row tiles per workgroup, K split in two
-    (13000, 256, 0.1),     # four row tiles per workgroup, ragged last workgroup
-    (40, 16384, 0.1),      # staging too large: the per-group fallback kernel
-    (100, 8192, 1.0),      # every group two-plane: records staged in several batches
+    (5000, 512, 0.1),      # one quad of groups (seven of eight waves get none), two row tiles per workgroup
+    (13000, 256, 0.1),     # half a quad; four row tiles (three with four column tiles), ragged last workgroup
+    (16400, 256, 0.05),    # four row tiles with up to three column tiles
+    (300, 10240, 0.1),     # three quads per wave, the last waves' quads past the end of K
+    (40, 16384, 0.1),      # four quads per wave, the most the registers allow
+    (40, 16896, 0.1),      # more quads per wave than that: the per-group fallback kernel
+    (100, 8192, 1.0),      # every group two-plane: over 512 records per workgroup, staged in several batches
 ])
 def test_workgroup_layouts(B, n_out, n_in, f2):
     log(f"smallbatch layout B={B} {n_out}x{n_in} f2={f2}")
@@ -78,7 +83,8 @@ def test_workgroup_layouts(B, n_out, n_in, f2):
 
 @pytest.mark.parametrize("B", [4, 16, 64])
 @pytest.mark.parametrize("n_out,n_in,f2", [
-    (12288, 4096, 0.036), (4096, 12288, 0.1), (5000, 512, 0.1), (40, 16384, 0.1), (100, 1024, 1.0),
+    (12288, 4096, 0.036), (4096, 12288, 0.1), (5000, 512, 0.1), (40, 16384, 0.1), (40, 16896, 0.1),
+    (100, 1024, 1.0),
 ])
 def test_group_offsets(B, n_out, n_in, f2):
     """Per-group offsets on every group, through every workgroup layout and
