@@ -256,7 +256,7 @@ def extra_suite(dev):
         inp = synth.projection(name, layer=0, cfg=4)
         base = tq.PackedLinear.from_inputs(inp, dev)
         mats = copies_of(base, ring)
-        for B in (1, 2, 4, 16, 64):
+        for B in (1, 2, 4, 8, 16, 32, 64):
             X = torch.from_numpy(synth.stage_activations(synth.STAGE_OF[name], layer=0, cfg=4, batch=B)).to(dev)
             Y = torch.empty(B, inp.n_out, dtype=torch.float16, device=dev)
             calls = [lambda m=m: tq.tq_gemm_smallbatch(m, X, Y=Y, stream=torch.cuda.current_stream()) for m in mats]
