@@ -15,7 +15,7 @@
 // byte 8u / 5) are fixed per step, known at compile time.
 //
 // Decode.  The GEMV's table (fp16 +-1/0 patterns (t0,t1), (t2,t3), (t4,0)
-// per code, 16 copies, at LDS address 0) is read once per code byte (a
+// per code, 16 copies, static LDS) is read once per code byte (a
 // byte shared by two windows is kept in registers); a window's four dwords
 // are table dwords or two of them joined by v_alignbit / v_lshl_or.  A
 // weight is pattern * s0 + offset in one v_pk_fma_f16 (exact without
@@ -27,11 +27,13 @@
 // Work split.  A workgroup of 8 waves owns 16 RT consecutive rows.  Its
 // waves split K by quads, and each wave covers all RT row tiles and all
 // batch columns, so a CU reads its slice of X once and decodes every weight
-// once.  Plane-0 codes go straight to registers, all loaded up front; X is
-// loaded a few pairs ahead of use.  The workgroup's plane-1 records are
-// staged in LDS with one slot per (row, group).  The waves' partial sums are
-// added in a fixed order through LDS (bit-reproducible).  Shapes beyond the
-// staging limits use the simple per-group kernel at the end of this file.
+// once.  Plane-0 codes go straight to registers, all loaded up front; X
+// comes in bursts of a whole line per lane, one burst ahead of use.  The
+// workgroup's plane-1 records are staged in LDS with one slot per (row,
+// group).  The waves' partial sums are added in a fixed order through LDS
+// (bit-reproducible).  Shapes past the register and LDS limits (more than
+// four quads per wave) use the simple per-group kernel at the end of this
+// file.
 
 #include "tq_internal.h"
 
@@ -47,7 +49,7 @@ constexpr int kLdsLimit = 160 * 1024;
 constexpr int kQWaves = 8;                       // waves per workgroup (K split)
 constexpr int kQThreads = 64 * kQWaves;
 constexpr int kQRep = 16;                        // table copies (lane & 15)
-constexpr int kQLutBytes = 256 * kQRep * 16;     // 64 KiB at LDS address 0
+constexpr int kQLutBytes = 256 * kQRep * 16;     // 64 KiB
 constexpr int kQMaxPairs = 2048;                 // record slots (rows x groups) per workgroup
 constexpr int kQMaxUnits = 4;                    // row tiles x quads per wave
 constexpr int kWindows = 16;                     // 8-input k blocks per group
@@ -67,8 +69,9 @@ struct QArgs {
   int out_f32;
 };
 
-// LDS: the table (static, at address 0, so a lane's table address needs no
-// base), then the dynamic part: row pointers [R + 1], record flags
+// LDS: the table (the kernel's only static array, so it sits at LDS address
+// 0 and the byte-to-address v_perm is the whole address; in the dynamic
+// block it cost an add per read), then the dynamic part: row pointers [R + 1], record flags
 // [R * G], record slots [R * G] x 32 B (byte offsets below); after the main
 // loop the partial sums [waves][RT][CT][64 lanes] x 16 B overlay it.
 __host__ __device__ constexpr int q_flag_off(int R) { return 4 * (R + 1); }
@@ -423,7 +426,7 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Fallback for shapes whose staging does not fit: per 128-wide K step, 64
+// Fallback for shapes past the quad kernel's limits: per 128-wide K step, 64
 // rows are decoded into an fp16 LDS tile in a 6-slots-per-byte order (the X
 // tile uses the same order) and multiplied with MFMA for every 16-column
 // slice of the batch.
