@@ -61,12 +61,17 @@ struct __attribute__((aligned(16))) U3 {
   uint32_t x, y, z;
 };
 
+constexpr int kQMaxRanges = 640;   // workgroups with record ranges in the kernel arguments
+
 struct QArgs {
   MatDev m;
   const uint16_t* X;
   void* Y;
   int B;
   int out_f32;
+  // With kHost: the first record of every workgroup, then nnz1 (from the
+  // host row pointers), so record loads need no dependent load.
+  int32_t rec_begin[kQMaxRanges + 1];
 };
 
 // LDS: the table (the kernel's only static array, so it sits at LDS address
@@ -185,7 +190,9 @@ __device__ inline RecLoad load_record(const MatDev& m, int64_t k) {
   return r;
 }
 
-template <int RT, int CT, int QPW>
+// kHost: the workgroup's record range comes from the kernel arguments
+// (host row pointers), so its record loads are issued before anything else.
+template <int RT, int CT, int QPW, bool kHost>
 __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
   __shared__ __attribute__((aligned(16))) unsigned char lut[kQLutBytes];
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
@@ -220,14 +227,39 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
 
   // ---- 1. Loads, all issued before any wait, every one unconditional at a
   // clamped address (a load whose destination is also written on another
-  // path forces an early wait).  Row pointers, the codes and scales of
-  // every (row tile, quad) of this wave, then the first steps' X.
+  // path forces an early wait).  With host ranges: the workgroup's first
+  // records (their range is known), the row pointers, the first X burst,
+  // then the codes and scales of every (row tile, quad) of this wave, so the
+  // record staging waits for the records alone while the codes stream in.
+  // Without: row pointers, codes, X, then the records once the device row
+  // pointers give their range.
   const int32_t* rp_src = has_rec ? m.rowptr1 : reinterpret_cast<const int32_t*>(m.codes0);
+  int kb = 0, ke = 0;
+  RecLoad rec0;
+  if constexpr (kHost) {
+    kb = a.rec_begin[blockIdx.x];
+    ke = a.rec_begin[blockIdx.x + 1];
+    rec0 = load_record(m, min(kb + tid, max(ke - 1, 0)));
+  }
   const int32_t rp_l = rp_src[row0 + min(tid, nrows)];
-  const int32_t kb_l = rp_src[row0];
-  const int32_t ke_l = rp_src[row0 + nrows];
   const uint16_t* off_src = has_off ? m.offset0 : m.scale0;
   const uint16_t* tail_src = reinterpret_cast<const uint16_t*>(m.codes0 + 24 * ngroups);
+
+  u4v xb[2][L][CT];
+  auto issue_x = [&](int v) {   // burst v: k-steps v L .. v L + L - 1 of this wave
+#pragma unroll
+    for (int k = 0; k < L; ++k) {
+      const int F = v * L + k;
+      const int qi = F / kWindows, u = F % kWindows;
+      const int g = min(4 * (wave * QPW + qi) + q, G - 1);
+#pragma unroll
+      for (int c = 0; c < CT; ++c) {
+        const int b = min(16 * c + r16, a.B - 1);
+        xb[v & 1][k][c] = *reinterpret_cast<const u4v*>(a.X + (int64_t)b * K + kGroup * g + 8 * u);
+      }
+    }
+  };
+  if constexpr (kHost) issue_x(0);
 
   uint32_t cw[QPW][RT][7];   // code bytes 0..23, then bytes 24, 25
   uint32_t sc[QPW][RT];      // s0 | offset << 16
@@ -250,27 +282,17 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
     }
   }
 
-  u4v xb[2][L][CT];
-  auto issue_x = [&](int v) {   // burst v: k-steps v L .. v L + L - 1 of this wave
-#pragma unroll
-    for (int k = 0; k < L; ++k) {
-      const int F = v * L + k;
-      const int qi = F / kWindows, u = F % kWindows;
-      const int g = min(4 * (wave * QPW + qi) + q, G - 1);
-#pragma unroll
-      for (int c = 0; c < CT; ++c) {
-        const int b = min(16 * c + r16, a.B - 1);
-        xb[v & 1][k][c] = *reinterpret_cast<const u4v*>(a.X + (int64_t)b * K + kGroup * g + 8 * u);
-      }
-    }
-  };
-  issue_x(0);
-
-  // The workgroup's first kQThreads plane-1 records, one per thread (a
-  // clamped in-range index where there are fewer; only threads below the
-  // count use theirs).
-  const int kb = has_rec ? kb_l : 0, ke = has_rec ? ke_l : 0;
-  const RecLoad rec0 = load_record(m, min(kb + tid, max(ke - 1, 0)));
+  if constexpr (!kHost) {
+    issue_x(0);
+    // The workgroup's first kQThreads plane-1 records, one per thread (a
+    // clamped in-range index where there are fewer; only threads below the
+    // count use theirs).
+    const int32_t kb_l = rp_src[row0];
+    const int32_t ke_l = rp_src[row0 + nrows];
+    kb = has_rec ? kb_l : 0;
+    ke = has_rec ? ke_l : 0;
+    rec0 = load_record(m, min(kb + tid, max(ke - 1, 0)));
+  }
 
   // ---- 2. Table (one code and half of its copies per thread; at step k
   // the copy index is rotated by the code so one store instruction's lanes
@@ -597,36 +619,37 @@ __global__ void __launch_bounds__(kThreads) fallback_kernel(MatDev m, const uint
 
 typedef void (*QKernel)(QArgs);
 
-template <int RT, int QPW>
+template <int RT, int QPW, bool H>
 QKernel q_pick(int CT) {
   switch (CT) {
-    case 1: return quad_kernel<RT, 1, QPW>;
-    case 2: return quad_kernel<RT, 2, QPW>;
-    case 3: return quad_kernel<RT, 3, QPW>;
+    case 1: return quad_kernel<RT, 1, QPW, H>;
+    case 2: return quad_kernel<RT, 2, QPW, H>;
+    case 3: return quad_kernel<RT, 3, QPW, H>;
     default:
       if constexpr (RT == 4) return nullptr;   // not launched: it would spill registers
-      else return quad_kernel<RT, 4, QPW>;
+      else return quad_kernel<RT, 4, QPW, H>;
   }
 }
 
 // (RT, QPW) pairs with RT * QPW <= kQMaxUnits.
+template <bool H>
 QKernel q_select(int RT, int QPW, int CT) {
   switch (RT) {
     case 1:
       switch (QPW) {
-        case 1: return q_pick<1, 1>(CT);
-        case 2: return q_pick<1, 2>(CT);
-        case 3: return q_pick<1, 3>(CT);
-        default: return q_pick<1, 4>(CT);
+        case 1: return q_pick<1, 1, H>(CT);
+        case 2: return q_pick<1, 2, H>(CT);
+        case 3: return q_pick<1, 3, H>(CT);
+        default: return q_pick<1, 4, H>(CT);
       }
-    case 2: return QPW == 1 ? q_pick<2, 1>(CT) : q_pick<2, 2>(CT);
-    case 3: return q_pick<3, 1>(CT);
-    default: return q_pick<4, 1>(CT);
+    case 2: return QPW == 1 ? q_pick<2, 1, H>(CT) : q_pick<2, 2, H>(CT);
+    case 3: return q_pick<3, 1, H>(CT);
+    default: return q_pick<4, 1, H>(CT);
   }
 }
 
 struct QDeviceInfo {
-  bool attr_set[4][4][4] = {};
+  bool attr_set[2][4][4][4] = {};
 };
 
 QDeviceInfo& q_device_info() {
@@ -661,17 +684,31 @@ hipError_t launch_gemm_smallbatch(const MatDev& m, const uint16_t* X, int B, voi
   const int staged = q_stage_bytes(R, G);
   const int red = q_red_bytes(RT, CT);
   const int dyn = staged > red ? staged : red;
-  const QKernel kern = q_select(RT, QPW, CT);
+  const int wgs = (m.n_out + R - 1) / R;
+  // Record ranges in the kernel arguments where the host has the row
+  // pointers (or there are no records) and the workgroups are few enough.
+  const bool host = (m.nnz1 == 0 || m.rowptr1_host != nullptr) && wgs <= kQMaxRanges;
+  const QKernel kern = host ? q_select<true>(RT, QPW, CT) : q_select<false>(RT, QPW, CT);
   if (kern == nullptr) return hipErrorInvalidValue;
   QDeviceInfo& di = q_device_info();
-  if (!di.attr_set[RT - 1][QPW - 1][CT - 1]) {
+  if (!di.attr_set[host][RT - 1][QPW - 1][CT - 1]) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, kLdsLimit - kQLutBytes);
     if (e != hipSuccess) return e;
-    di.attr_set[RT - 1][QPW - 1][CT - 1] = true;
+    di.attr_set[host][RT - 1][QPW - 1][CT - 1] = true;
   }
-  QArgs args{m, X, Y, B, out_f32 ? 1 : 0};
-  const int wgs = (m.n_out + R - 1) / R;
+  QArgs args;
+  args.m = m;
+  args.X = X;
+  args.Y = Y;
+  args.B = B;
+  args.out_f32 = out_f32 ? 1 : 0;
+  if (host) {
+    for (int w = 0; w <= wgs; ++w) {
+      const int64_t r = (int64_t)w * R < m.n_out ? (int64_t)w * R : m.n_out;
+      args.rec_begin[w] = m.nnz1 > 0 ? m.rowptr1_host[r] : 0;
+    }
+  }
   hipLaunchKernelGGL(kern, dim3(wgs), dim3(kQThreads), dyn, s, args);
   return hipGetLastError();
 }
