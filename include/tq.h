@@ -103,10 +103,12 @@ typedef struct tq_matrix {
   const uint16_t* offset1;
   const uint16_t* scale1;
   /* Optional (may be NULL): a HOST copy of rowptr1, read during the call
-   * only.  With it the GEMV finds every workgroup's records on the host and
-   * issues their loads with its first batch, instead of reading the device
-   * row pointers first.  It must hold the same values as rowptr1; if it does
-   * not, results are unspecified, but every access stays in bounds. */
+   * only.  With it the GEMV and the small-batch kernels find every
+   * workgroup's records on the host and issue their loads with their first
+   * batch, instead of reading the device row pointers first (B = 2..4 use
+   * the GEMV's decode only when it is present).  It must hold the same
+   * values as rowptr1; if it does not, results are unspecified, but every
+   * access stays in bounds. */
   const int32_t* rowptr1_host;
   /* Optional (may be NULL; ABI 3): fp16 [N][G] offset mu0 of EVERY group,
    * the paper's representation (eq. 3 gives every masked block an offset).
