@@ -81,6 +81,22 @@ def test_workgroup_layouts(B, n_out, n_in, f2):
     log(f"  max err/bound {r:.3g}")
 
 
+@pytest.mark.parametrize("B", [17, 40, 64])
+@pytest.mark.parametrize("n_out,n_in,f2", [(5000, 512, 0.1), (300, 10240, 0.1), (100, 8192, 1.0)])
+def test_without_host_row_pointers(B, n_out, n_in, f2):
+    """Without the host row pointers the MFMA kernel reads each workgroup's
+    record range from the device row pointers (after the codes): same
+    results within the bound, for several column tiles and more than 512
+    records per workgroup."""
+    log(f"smallbatch device ranges B={B} {n_out}x{n_in} f2={f2}")
+    inp = synth.linear(n_out, n_in, f2, (23, n_out, n_in, B))
+    X = synth.activations(n_in, (23, n_out, n_in, 96), batch=B, outlier_frac=0.01)
+    case = Case(inp, host_rowptr=False)
+    got = run(case, X, out_f32=True)
+    r = assert_within_bound(got, case.oracle_gemm(X), case.bound(X), f"device ranges B={B} {n_out}x{n_in}")
+    log(f"  max err/bound {r:.3g}")
+
+
 @pytest.mark.parametrize("B", [4, 16, 64])
 @pytest.mark.parametrize("n_out,n_in,f2", [
     (12288, 4096, 0.036), (4096, 12288, 0.1), (5000, 512, 0.1), (40, 16384, 0.1), (40, 16896, 0.1),
