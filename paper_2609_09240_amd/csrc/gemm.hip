@@ -197,13 +197,19 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
   __shared__ __attribute__((aligned(16))) unsigned char lut[kQLutBytes];
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   constexpr int R = 16 * RT;
-  // X is loaded in bursts of L consecutive chunks per lane (a whole
-  // 128-byte line, or half of one when four column tiles leave too few
-  // registers), one burst ahead of use: every line is fetched once and used
-  // whole.  Single 16-byte chunks per step made each line be refetched for
-  // every chunk: the 16 batch rows of a step lie a power-of-two stride apart
-  // and evict each other from L1.
-  constexpr int L = CT <= 2 ? 8 : 4;
+  // X is loaded in bursts of L consecutive chunks per lane, a whole 128-byte
+  // line, so every line is fetched once and used whole.  Single 16-byte
+  // chunks per step made each line be refetched for every chunk: the 16
+  // batch rows of a step lie a power-of-two stride apart and evict each
+  // other from L1.  With up to two column tiles the next burst is loaded
+  // while the current one is used (NB = 2 buffers).  Three or four column
+  // tiles leave registers for one line buffer only: with several quads per
+  // wave it is refilled after each block (whole lines, the latency exposed
+  // once per 8 steps); with one quad, half-line bursts in two buffers are
+  // faster (gate 12288x4096 at B = 64: 28 against 31 us; down 4096x12288:
+  // 57 against 55 us the other way round).
+  constexpr int L = (CT <= 2 || QPW >= 2) ? 8 : 4;
+  constexpr int NB = (CT <= 2 || QPW == 1) ? 2 : 1;
   constexpr int NW = QPW * kWindows;      // k-steps of this wave
 
   const MatDev& m = a.m;
@@ -245,7 +251,7 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
   const uint16_t* off_src = has_off ? m.offset0 : m.scale0;
   const uint16_t* tail_src = reinterpret_cast<const uint16_t*>(m.codes0 + 24 * ngroups);
 
-  u4v xb[2][L][CT];
+  u4v xb[NB][L][CT];
   auto issue_x = [&](int v) {   // burst v: k-steps v L .. v L + L - 1 of this wave
 #pragma unroll
     for (int k = 0; k < L; ++k) {
@@ -255,7 +261,7 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
 #pragma unroll
       for (int c = 0; c < CT; ++c) {
         const int b = min(16 * c + r16, a.B - 1);
-        xb[v & 1][k][c] = *reinterpret_cast<const u4v*>(a.X + (int64_t)b * K + kGroup * g + 8 * u);
+        xb[v % NB][k][c] = *reinterpret_cast<const u4v*>(a.X + (int64_t)b * K + kGroup * g + 8 * u);
       }
     }
   };
@@ -377,11 +383,11 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
 #pragma unroll
     for (int v = 0; v < kWindows / L; ++v) {
     const int F0 = qi * kWindows + v * L;
-    if (F0 + L < NW) issue_x(F0 / L + 1);
+    if (NB == 2 && F0 + L < NW) issue_x(F0 / L + 1);
 #pragma unroll
     for (int k = 0; k < L; ++k) {
       const int u = v * L + k, F = F0 + k;
-      const u4v (&xv)[CT] = xb[(F / L) & 1][k];
+      const u4v (&xv)[CT] = xb[(F / L) % NB][k];
       const int j0 = win_byte(u), jl = win_last(u);
       const bool shared = u > 0 && win_last(u - 1) == j0;   // first byte already read
 #pragma unroll
@@ -411,6 +417,7 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
           acc[rt][c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, __builtin_bit_cast(half8, xv[c]), acc[rt][c], 0, 0, 0);
       }
     }
+    if (NB == 1 && F0 + L < NW) issue_x(F0 / L + 1);
     }
   }
 
