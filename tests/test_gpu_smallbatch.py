@@ -61,6 +61,17 @@ def test_deterministic():
     assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
 
 
+@pytest.mark.parametrize("name,B", [("gate", 64), ("down", 16), ("down", 40)])
+def test_deterministic_mlp_shapes(name, B):
+    """The eight waves' partial sums over K are added in a fixed order, so
+    repeated calls give the same bits (fp32 output) at the MLP shapes."""
+    case = Case(synth.projection(name, layer=3, cfg=4))
+    X = synth.stage_activations(synth.STAGE_OF[name], layer=3, cfg=4, batch=B)
+    first = run(case, X, True)
+    for _ in range(2):
+        assert np.array_equal(first.view(np.uint32), run(case, X, True).view(np.uint32))
+
+
 @pytest.mark.parametrize("B", [3, 16, 40, 64])
 @pytest.mark.parametrize("n_out,n_in,f2", [
     (5000, 512, 0.1),      # one quad of groups (seven of eight waves get none), two row tiles per workgroup
