@@ -302,11 +302,8 @@ def extra_suite(dev):
     s0b = torch.empty(ng, dtype=torch.float16, device=dev)
     eb = torch.empty(ng, dtype=torch.float64, device=dev)
     t_rank = graph_time_us([lambda: tq.tq_ternarize(groups, iters=0, t0=t0b, s0=s0b, energy=eb)] * 4)
-    sel = tq.select_two_plane(eb.cpu().numpy(), 0.1)
-    nnz = int(sel.size)
-    rec = np.full(ng, -1, dtype=np.int32)
-    rec[sel] = np.arange(nnz, dtype=np.int32)
-    rec_d = torch.from_numpy(rec).to(dev)
+    nnz = int(np.floor(0.1 * ng))
+    rec_d = tq.tq_select_two_plane(eb, N, K // 128, nnz)[0]
     t1b = torch.empty((nnz, 128), dtype=torch.int8, device=dev)
     mub = torch.empty(nnz, dtype=torch.float16, device=dev)
     s1b = torch.empty(nnz, dtype=torch.float16, device=dev)

@@ -59,13 +59,14 @@
 #ifndef TQ_H
 #define TQ_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
 extern "C" {
 #endif
 
-#define TQ_ABI_VERSION 4
+#define TQ_ABI_VERSION 5
 #define TQ_GROUP 128
 #define TQ_GROUP_BYTES 26
 #define TQ_MAX_GROUPS_PER_ROW 256    /* K <= 32768 */
@@ -143,7 +144,11 @@ tq_status tq_unpack(const uint8_t* codes, int64_t n_groups, int32_t group,
                     int8_t* trits, int32_t* d_err, void* stream);
 
 /* Count invalid bytes of a code buffer into *d_err (required here): codes
- * above 242, and last bytes (byte 25) whose pad digits are not both 1. */
+ * above 242, and last bytes (byte 25) whose pad digits are not both 1.
+ * Section 12 makes the packed buffer the lossless carrier of the discrete
+ * supports; section 5.4 reports malformed packed tensors that still gave
+ * plausible-looking numbers, and section 15 lists such artifact failures.
+ * So a loader checks a buffer once with this call; the GEMV does not. */
 tq_status tq_validate(const uint8_t* codes, int64_t n_groups, int32_t group,
                       int32_t* d_err, void* stream);
 
@@ -169,7 +174,9 @@ tq_status tq_gemv(const tq_matrix* m, const uint16_t* x, void* y,
                   int32_t flags, void* stream);
 
 /* Several GEMVs that read the same x in one launch (e.g. q, k and v, or
- * gate and up of one decoder layer).
+ * gate and up of one decoder layer).  Section 13 measures the packed decode
+ * step of a whole model; in a decoder layer q, k, v read the same normalised
+ * input and so do gate and up, so one launch serves each pair or triple.
  *   ms  host array of n matrices (1 <= n <= TQ_MAX_GROUPED), all with the
  *       same K
  *   ys  host array of n device output pointers, ys[i] of N_i elements
@@ -224,6 +231,38 @@ tq_status tq_ternarize(const uint16_t* w, int64_t n_groups, int32_t group,
                        int8_t* t0, uint16_t* s0, int8_t* t1, uint16_t* offset1,
                        uint16_t* scale1, uint16_t* offset0, double* energy,
                        void* stream);
+
+/* Bytes of device workspace tq_select_two_plane needs for n_groups groups
+ * (host function; 0 for n_groups < 0). */
+size_t tq_select_workspace_bytes(int64_t n_groups);
+
+/* The two-plane groups of a linear and its plane-1 CSR (ABI 5).  Section
+ * 4.2 gives a second ternary plane to a minority of blocks; section 3
+ * chooses them with salience masks fitted on calibration activations, so
+ * without calibration data the ranking is each group's one-plane residual
+ * energy (tq_ternarize's `energy`).  The call selects the nnz groups with
+ * the largest energy, ties to the lower flat index (groups in row-major
+ * (r, g) order); a NaN energy ranks below every number, -0 and +0 tie.
+ * Records are numbered in flat order, which is the CSR order by row.
+ *   energy          fp64 [n_out * groups_per_row]; 8-byte aligned
+ *   n_out >= 1, 1 <= groups_per_row <= TQ_MAX_GROUPS_PER_ROW,
+ *   n_out * groups_per_row < 2^31
+ *   nnz             0 <= nnz <= n_out * groups_per_row
+ *   rec_index       int32 [n_out * groups_per_row] out: the record of each
+ *                   group, -1 for one-plane groups (tq_ternarize's input)
+ *   rowptr1         int32 [n_out + 1] out (tq_matrix.rowptr1)
+ *   gidx1           uint16 [nnz] out (tq_matrix.gidx1); may be NULL when
+ *                   nnz == 0
+ *   workspace       device scratch of workspace_bytes >=
+ *                   tq_select_workspace_bytes(n_out * groups_per_row)
+ *                   bytes, 256-byte aligned; its contents on entry do not
+ *                   matter and on return are unspecified.  Two calls that
+ *                   share a workspace must not overlap in time.
+ * All pointers are device memory; 4-byte alignment for rec_index and
+ * rowptr1, 2-byte for gidx1.  The result is deterministic and unique. */
+tq_status tq_select_two_plane(const double* energy, int64_t n_out, int32_t groups_per_row, int64_t nnz,
+                              int32_t* rec_index, int32_t* rowptr1, uint16_t* gidx1,
+                              void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -178,7 +178,8 @@ __device__ inline RecLoad load_record(const MatDev& m, int64_t k) {
   const uint16_t* mu = has ? m.offset1 : m.scale0;
   const uint16_t* s1 = has ? m.scale1 : m.scale0;
   const uint16_t* gi = has ? m.gidx1 : m.scale0;
-  k = has ? k : 0;
+  // In bounds whatever range the caller's row pointers give.
+  k = has ? (k < 0 ? 0 : (k >= n ? n - 1 : k)) : 0;
   const uint64_t* rm = reinterpret_cast<const uint64_t*>(codes) + 3 * k;
   RecLoad r;
   r.v0 = rm[0];
@@ -713,7 +714,9 @@ hipError_t launch_gemm_smallbatch(const MatDev& m, const uint16_t* X, int B, voi
   if (host) {
     for (int w = 0; w <= wgs; ++w) {
       const int64_t r = (int64_t)w * R < m.n_out ? (int64_t)w * R : m.n_out;
-      args.rec_begin[w] = m.nnz1 > 0 ? m.rowptr1_host[r] : 0;
+      int64_t v = m.nnz1 > 0 ? m.rowptr1_host[r] : 0;
+      v = v < 0 ? 0 : (v > m.nnz1 ? m.nnz1 : v);   // in bounds whatever the host copy holds
+      args.rec_begin[w] = (int32_t)v;
     }
   }
   hipLaunchKernelGGL(kern, dim3(wgs), dim3(kQThreads), dyn, s, args);

@@ -185,4 +185,26 @@ tq_status tq_ternarize(const uint16_t* w, int64_t n_groups, int32_t group, const
                                        energy, (hipStream_t)stream));
 }
 
+size_t tq_select_workspace_bytes(int64_t n_groups) {
+  if (n_groups < 0) return 0;
+  return tq::select_workspace_bytes(n_groups);
+}
+
+tq_status tq_select_two_plane(const double* energy, int64_t n_out, int32_t groups_per_row, int64_t nnz,
+                              int32_t* rec_index, int32_t* rowptr1, uint16_t* gidx1, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  if (n_out < 1 || groups_per_row < 1 || groups_per_row > TQ_MAX_GROUPS_PER_ROW) return TQ_ERR_SHAPE;
+  if (n_out > (int64_t)INT32_MAX / groups_per_row) return TQ_ERR_SHAPE;
+  const int64_t n = n_out * groups_per_row;
+  if (nnz < 0 || nnz > n) return TQ_ERR_SHAPE;
+  if (energy == nullptr || rec_index == nullptr || rowptr1 == nullptr || workspace == nullptr) return TQ_ERR_NULL;
+  if (nnz > 0 && gidx1 == nullptr) return TQ_ERR_NULL;
+  if (workspace_bytes < tq::select_workspace_bytes(n)) return TQ_ERR_SHAPE;
+  if (misaligned(energy, 8) || misaligned(rec_index, 4) || misaligned(rowptr1, 4) || misaligned(workspace, 256) ||
+      (gidx1 != nullptr && misaligned(gidx1, 2)))
+    return TQ_ERR_ALIGN;
+  return from_hip(tq::launch_select(energy, n_out, groups_per_row, nnz, rec_index, rowptr1, gidx1, workspace,
+                                    (hipStream_t)stream));
+}
+
 }  // extern "C"

@@ -57,4 +57,10 @@ hipError_t launch_ternarize(const uint16_t* w, int64_t n_groups, const int32_t* 
                             int iters, int8_t* t0, uint16_t* s0, int8_t* t1, uint16_t* offset1,
                             uint16_t* scale1, uint16_t* offset0, double* energy, hipStream_t s);
 
+// Two-plane selection and plane-1 CSR (select.hip); workspace of
+// select_workspace_bytes(n_out * G) bytes, 256-byte aligned.
+size_t select_workspace_bytes(int64_t n_groups);
+hipError_t launch_select(const double* energy, int64_t n_out, int32_t G, int64_t nnz, int32_t* rec_index,
+                         int32_t* rowptr1, uint16_t* gidx1, void* workspace, hipStream_t s);
+
 }  // namespace tq

@@ -16,7 +16,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtq.so")
 
-ABI_VERSION = 4
+ABI_VERSION = 5
 GROUP = 128
 GROUP_BYTES = 26
 OUT_FP16 = 0
@@ -76,6 +76,8 @@ def lib():
             "tq_gemv_grouped": ([mp, i32, vp, ctypes.POINTER(ctypes.c_void_p), i32, vp], ctypes.c_int),
             "tq_gemm_smallbatch": ([mp, vp, i32, vp, i32, vp], ctypes.c_int),
             "tq_ternarize": ([vp, i64, i32, vp, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp], ctypes.c_int),
+            "tq_select_workspace_bytes": ([i64], ctypes.c_size_t),
+            "tq_select_two_plane": ([vp, i64, i32, i64, vp, vp, vp, vp, ctypes.c_size_t, vp], ctypes.c_int),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(L, name)
@@ -95,6 +97,30 @@ def _ptr(t):
 def _stream(stream):
     s = torch.cuda.current_stream() if stream is None else stream
     return ctypes.c_void_p(s.cuda_stream)
+
+
+def _used_on(stream, *tensors):
+    """Tensors that a launch on `stream` reads or writes: when that is not the
+    current stream, tell the caching allocator not to reuse their memory
+    before the stream's work is done."""
+    if stream is not None and stream != torch.cuda.current_stream():
+        for t in tensors:
+            if t is not None:
+                t.record_stream(stream)
+
+
+def _after_current(stream):
+    """Order `stream` after the work queued so far on the current stream
+    (uploads made with .to(device) run there)."""
+    if stream is not None and stream != torch.cuda.current_stream():
+        stream.wait_stream(torch.cuda.current_stream())
+
+
+def _host_copy(t, stream):
+    """Host copy of a device tensor written on `stream`."""
+    if stream is not None:
+        torch.cuda.current_stream().wait_stream(stream)
+    return t.cpu()
 
 
 def _check(status, where):
@@ -169,11 +195,15 @@ class PackedLinear:
         tq_matrix.rowptr1_host)."""
         dev = torch.device(device)
         t0 = torch.from_numpy(inp.t0.reshape(-1, GROUP)).to(dev)
+        _after_current(stream)
         codes0 = tq_pack(t0, stream=stream)
+        _used_on(stream, t0)
         del t0
         kw = {}
         if inp.nnz1:
             t1 = torch.from_numpy(inp.t1.reshape(-1, GROUP)).to(dev)
+            _after_current(stream)
+            _used_on(stream, t1)
             kw = dict(
                 rowptr1=torch.from_numpy(inp.rowptr1).to(dev),
                 gidx1=torch.from_numpy(inp.gidx1.view("int16")).to(dev),
@@ -310,53 +340,65 @@ def tq_ternarize(w, rec_index=None, nnz=0, iters=4, t0=None, s0=None, t1=None, o
     return t0, s0, t1, offset1, scale1, energy, offset0
 
 
-def select_two_plane(energy, f2):
-    """Host rule for the two-plane subset: the floor(f2 * n) groups with the
-    largest one-plane residual energy, ties to the lower flat index; returns
-    their sorted flat indices (numpy int64)."""
-    import numpy as np
-    e = np.asarray(energy, dtype=np.float64)
-    n = e.size
-    k = int(np.floor(f2 * n))
-    order = np.lexsort((np.arange(n), -e))
-    return np.sort(order[:k])
+def tq_select_workspace_bytes(n_groups):
+    return int(lib().tq_select_workspace_bytes(n_groups))
+
+
+def tq_select_two_plane(energy, n_out, groups_per_row, nnz, rec_index=None, rowptr1=None, gidx1=None,
+                        workspace=None, stream=None):
+    """The nnz groups with the largest energy (fp64 [n_out * groups_per_row],
+    on the GPU), ties to the lower flat index, and their plane-1 CSR: returns
+    (rec_index int32 [n], rowptr1 int32 [n_out + 1], gidx1 int16 [nnz] holding
+    uint16 group indices)."""
+    _cuda(energy, torch.float64, "energy")
+    n = n_out * groups_per_row
+    dev = energy.device
+    if rec_index is None:
+        rec_index = torch.empty(n, dtype=torch.int32, device=dev)
+    if rowptr1 is None:
+        rowptr1 = torch.empty(n_out + 1, dtype=torch.int32, device=dev)
+    if gidx1 is None:
+        gidx1 = torch.empty(nnz, dtype=torch.int16, device=dev)
+    if workspace is None:
+        workspace = torch.empty(tq_select_workspace_bytes(n), dtype=torch.uint8, device=dev)
+    _check(lib().tq_select_two_plane(_ptr(energy), n_out, groups_per_row, nnz, _ptr(rec_index), _ptr(rowptr1),
+                                     _ptr(gidx1) if nnz else None, _ptr(workspace), workspace.numel(),
+                                     _stream(stream)), "tq_select_two_plane")
+    _used_on(stream, energy, rec_index, rowptr1, gidx1, workspace)
+    return rec_index, rowptr1, gidx1
 
 
 def quantize_linear(W, f2=0.1, iters=4, host_rowptr=True, group_offsets=False, stream=None):
     """Packed linear from dense fp16 weights W [N, K] on the GPU: one-plane
-    fits rank the groups, the top f2 get two planes, then tq_ternarize and
-    tq_pack produce the stored planes (section 4.2 and section 12).  With
-    ``group_offsets`` every group carries an offset (offset0), the paper's
-    own representation of section 3, eq. 3."""
-    import numpy as np
+    fits rank the groups (tq_ternarize), the top floor(f2 * N * K / 128) get
+    two planes (tq_select_two_plane), then tq_ternarize and tq_pack produce
+    the stored planes (section 4.2 and section 12).  With ``group_offsets``
+    every group carries an offset (offset0), the paper's own representation
+    of section 3, eq. 3."""
+    import math
     _cuda(W, torch.float16, "W")
     N, K = W.shape
     if K % GROUP:
         raise ValueError("K must be a multiple of 128")
     ng = K // GROUP
     groups = W.reshape(N * ng, GROUP)
+    _after_current(stream)
     # The ranking fit: with offsets its refinement decides the energy.
-    energy = tq_ternarize(groups, iters=iters if group_offsets else 0, group_offsets=group_offsets,
-                          stream=stream)[5]
-    sel = select_two_plane(energy.cpu().numpy(), f2)
-    nnz = int(sel.size)
-    rec = np.full(N * ng, -1, dtype=np.int32)
-    rec[sel] = np.arange(nnz, dtype=np.int32)
-    rowptr = np.zeros(N + 1, dtype=np.int32)
-    np.add.at(rowptr, sel // ng + 1, 1)
-    rowptr = np.cumsum(rowptr).astype(np.int32)
-    dev = W.device
-    t0, s0, t1, mu, s1, _, mu0 = tq_ternarize(groups, rec_index=torch.from_numpy(rec).to(dev), nnz=nnz,
-                                              iters=iters, want_energy=False, group_offsets=group_offsets,
-                                              stream=stream)
+    ranking = tq_ternarize(groups, iters=iters if group_offsets else 0, group_offsets=group_offsets,
+                           stream=stream)
+    energy = ranking[5]
+    nnz = int(math.floor(f2 * N * ng))
+    rec, rowptr, gidx = tq_select_two_plane(energy, N, ng, nnz, stream=stream)
+    _used_on(stream, groups, *[t for t in ranking if t is not None])
+    t0, s0, t1, mu, s1, _, mu0 = tq_ternarize(groups, rec_index=rec, nnz=nnz, iters=iters, want_energy=False,
+                                              group_offsets=group_offsets, stream=stream)
     codes0 = tq_pack(t0, stream=stream)
+    _used_on(stream, rec, t0, t1, s0, mu, s1, mu0)
     kw = {}
     if nnz:
-        kw = dict(rowptr1=torch.from_numpy(rowptr).to(dev),
-                  gidx1=torch.from_numpy((sel % ng).astype(np.uint16).view(np.int16)).to(dev),
-                  codes1=tq_pack(t1, stream=stream), offset1=mu, scale1=s1)
+        kw = dict(rowptr1=rowptr, gidx1=gidx, codes1=tq_pack(t1, stream=stream), offset1=mu, scale1=s1)
         if host_rowptr:
-            kw["rowptr1_host"] = torch.from_numpy(rowptr).contiguous()
+            kw["rowptr1_host"] = _host_copy(rowptr, stream).contiguous()
     if group_offsets:
         kw["offset0"] = mu0.reshape(N, ng)
     return PackedLinear(N, K, codes0, s0.reshape(N, ng), **kw)

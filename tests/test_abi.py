@@ -32,7 +32,8 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for want in ["tq_pack", "tq_unpack", "tq_validate", "tq_unpack_fp16", "tq_gemv", "tq_gemv_grouped",
-                 "tq_gemm_smallbatch", "tq_ternarize", "tq_status_string", "tq_abi_version"]:
+                 "tq_gemm_smallbatch", "tq_ternarize", "tq_status_string", "tq_abi_version",
+                 "tq_select_workspace_bytes", "tq_select_two_plane"]:
         assert want in names
 
 
@@ -43,7 +44,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert tq.tq_abi_version() == tq.ABI_VERSION == 4
+    assert tq.tq_abi_version() == tq.ABI_VERSION == 5
     for s in range(6):
         assert tq.tq_status_string(s).startswith(tq.STATUS[s])
     assert "unknown" in tq.tq_status_string(42)
@@ -168,6 +169,37 @@ def test_ternarize_rejects_bad_arguments():
     assert call(w=v(FAKE + 8)) == 3 and call(t0=v(FAKE + 4)) == 3 and call(s0=v(FAKE + 1)) == 3
     assert call(rec=v(FAKE + 2)) == 3 and call(e=v(FAKE + 4)) == 3 and call(m0=v(FAKE + 1)) == 3
     assert call(nnz=3, t1=v(FAKE + 8), mu=F, s1=F) == 3
+
+
+def test_select_workspace_size():
+    """Histogram and state, then four counters per tile of 4096 groups,
+    rounded up to 256 bytes."""
+    f = tq.lib().tq_select_workspace_bytes
+    assert f(-1) == 0
+    for n in (0, 1, 4096, 4097, 393216, 2 ** 31 - 1):
+        tiles = (n + 4095) // 4096
+        want = 1024 + 32 + 16 * tiles
+        assert f(n) == (want + 255) // 256 * 256, n
+
+
+@no_gpu
+def test_select_rejects_bad_arguments():
+    L = tq.lib()
+    v = ctypes.c_void_p
+    F = v(FAKE)
+    ws = tq.lib().tq_select_workspace_bytes(64 * 32)
+
+    def call(e=F, n_out=64, G=32, nnz=10, rec=F, rp=F, gi=F, w=F, wb=ws):
+        return L.tq_select_two_plane(e, n_out, G, nnz, rec, rp, gi, w, wb, None)
+
+    assert call(n_out=0) == 2 and call(G=0) == 2 and call(G=257) == 2
+    assert call(n_out=2 ** 31 // 32 + 1) == 2                         # more than 2^31 - 1 groups
+    assert call(nnz=-1) == 2 and call(nnz=64 * 32 + 1) == 2
+    assert call(e=None) == 1 and call(rec=None) == 1 and call(rp=None) == 1 and call(w=None) == 1
+    assert call(gi=None) == 1                                         # needed when nnz > 0
+    assert call(wb=ws - 1) == 2                                       # workspace too small
+    assert call(e=v(FAKE + 4)) == 3 and call(rec=v(FAKE + 2)) == 3 and call(rp=v(FAKE + 2)) == 3
+    assert call(gi=v(FAKE + 1)) == 3 and call(w=v(FAKE + 128)) == 3
 
 
 def test_binding_refuses_cpu_tensors():

@@ -181,3 +181,19 @@ def test_few_rows_group_offsets(B, n_out, n_in, f2):
         torch.cuda.synchronize()
         assert np.array_equal(got[b], y.cpu().numpy())
     log(f"few rows offsets B={B} {n_out}x{n_in}: max err/bound {r:.3g}")
+
+
+@pytest.mark.parametrize("B,shift", [(5, 7), (16, -5), (40, 10 ** 6), (3, 10 ** 6)])
+def test_bad_host_rowptr_stays_in_bounds(B, shift):
+    """A host copy of the row pointers that differs from the device copy
+    (shifted, or far past nnz1) gives unspecified values but every access
+    stays in bounds: the call completes and the output is finite."""
+    case = Case(synth.linear(700, 1024, 0.1, (13, B, 0, 0)))
+    good = case.gpu.rowptr1_host.clone()
+    case.gpu.rowptr1_host = (good.to(torch.int64) + shift).clamp(-(2 ** 31), 2 ** 31 - 1).to(torch.int32)
+    X = synth.activations(1024, (13, B, 0, 1), batch=B)
+    got = run(case, X, out_f32=True)
+    assert np.all(np.isfinite(got))
+    case.gpu.rowptr1_host = good
+    want = case.oracle_gemm(X)
+    assert_within_bound(run(case, X, out_f32=True), want, case.bound(X), f"B={B} after restoring rowptr")

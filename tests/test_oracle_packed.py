@@ -296,3 +296,122 @@ def test_dense_fp16_with_group_offsets():
         for c in range(512):
             if not two[r, c // 128] and inp.t0[r, c] == 0:
                 assert w16[r, c] == inp.mu0[r, c // 128]
+
+
+# ---------------------------------------------------------------------------
+# The acceptance bound, pinned from above and below by closed forms (reading
+# of the accuracy bound: per output, 2e-3 * sum_g coef[r, g] * ||x_g||_1 with
+# coef = |s0| (+ |mu0|) (+ |mu| + |s1| on two-plane groups)).
+# ---------------------------------------------------------------------------
+
+def _hand_case(with_offsets):
+    """Two rows, two groups (K = 256); one record, on (row 0, group 1).
+    Values are dyadic, so every bound below is exact in fp64 up to the final
+    multiplication by 2e-3."""
+    s0 = np.array([[0.5, 0.25], [1.0, 2.0]], np.float16)
+    rowptr1 = np.array([0, 1, 1], np.int32)
+    gidx1 = np.array([1], np.uint16)
+    mu1 = np.array([-0.125], np.float16)
+    s1 = np.array([0.75], np.float16)
+    mu0 = np.array([[0.5, -0.25], [0.0, 0.0]], np.float16) if with_offsets else None
+    x = np.zeros(256, np.float16)
+    x[:128] = 1.0                 # ||x_0||_1 = 128
+    x[200] = -2.0                 # ||x_1||_1 = 2
+    return s0, rowptr1, gidx1, mu1, s1, mu0, x
+
+
+def bound_pin_failures(bound):
+    """Names of the closed-form pins that `bound` (a callable with the
+    signature of packed.error_bound) fails."""
+    fails = []
+    rel = 2e-3
+
+    # Hand-worked case, written out from the reading above.
+    s0, rowptr1, gidx1, mu1, s1, _, x = _hand_case(False)
+    got = bound(2, 256, s0, rowptr1, gidx1, mu1, s1, x)
+    # row 0: 0.5*128 + (0.25 + 0.125 + 0.75)*2 = 66.25 ; row 1: 1*128 + 2*2 = 132
+    if not np.allclose(got, [rel * 66.25, rel * 132.0], rtol=1e-14, atol=0):
+        fails.append("hand case")
+    s0, rowptr1, gidx1, mu1, s1, mu0, x = _hand_case(True)
+    got = bound(2, 256, s0, rowptr1, gidx1, mu1, s1, x, offset0=mu0)
+    # row 0 adds |mu0|: 0.5*128 + 0.25*2 = 64.5 -> 130.75 ; row 1 unchanged
+    if not np.allclose(got, [rel * 130.75, rel * 132.0], rtol=1e-14, atol=0):
+        fails.append("hand case with offsets")
+
+    # x == 1, one plane: 2e-3 * 128 * sum_g |s0|.
+    rng = np.random.default_rng(5)
+    n, k = 5, 640
+    s0 = (rng.uniform(-0.05, 0.05, (n, k // 128))).astype(np.float16)
+    ones = np.ones(k, np.float16)
+    got = bound(n, k, s0, None, None, None, None, ones)
+    want = rel * 128 * np.abs(s0.astype(np.float64)).sum(axis=1)
+    if not np.allclose(got, want, rtol=1e-14, atol=0):
+        fails.append("x == 1, one plane")
+
+    # x == 1 with records: + 128 (|mu| + |s1|) per record group.
+    rowptr1 = np.array([0, 2, 2, 3, 3, 5], np.int32)
+    gidx1 = np.array([0, 4, 2, 1, 3], np.uint16)
+    mu1 = rng.uniform(-0.01, 0.01, 5).astype(np.float16)
+    s1 = rng.uniform(0.01, 0.05, 5).astype(np.float16)
+    got = bound(n, k, s0, rowptr1, gidx1, mu1, s1, ones)
+    want = want.copy()
+    rows = np.repeat(np.arange(n), np.diff(rowptr1))
+    for j, r in enumerate(rows):
+        want[r] += rel * 128 * (abs(float(mu1[j])) + abs(float(s1[j])))
+    if not np.allclose(got, want, rtol=1e-14, atol=0):
+        fails.append("x == 1 with records")
+
+    # x = e_k: the coefficient of column k's group only.
+    mu0 = rng.uniform(-0.01, 0.01, (n, k // 128)).astype(np.float16)
+    for col in (0, 127, 128, 300, 639):
+        e = np.zeros(k, np.float16)
+        e[col] = 1.0
+        got = bound(n, k, s0, rowptr1, gidx1, mu1, s1, e, offset0=mu0)
+        g = col // 128
+        want = np.abs(s0[:, g].astype(np.float64)) + np.abs(mu0[:, g].astype(np.float64))
+        for j, r in enumerate(rows):
+            if int(gidx1[j]) == g:
+                want[r] += abs(float(mu1[j])) + abs(float(s1[j]))
+        if not np.allclose(got, rel * want, rtol=1e-14, atol=0):
+            fails.append(f"x = e_{col}")
+    return fails
+
+
+def test_error_bound_closed_forms():
+    assert bound_pin_failures(packed.error_bound) == []
+
+
+def _planted_bound(mistake):
+    def bound(n_out, n_in, scale0, rowptr1, gidx1, offset1, scale1, X, rel=2e-3, offset0=None):
+        ng = n_in // 128
+        coef = np.abs(np.asarray(scale0, np.float16).astype(np.float64)).reshape(n_out, ng)
+        if offset0 is not None:
+            coef = coef + np.abs(np.asarray(offset0, np.float16).astype(np.float64)).reshape(n_out, ng)
+        nnz = 0 if gidx1 is None else int(np.asarray(gidx1).size)
+        if nnz:
+            rows = np.repeat(np.arange(n_out), np.diff(np.asarray(rowptr1, np.int64)))
+            g = np.asarray(gidx1).astype(np.int64)
+            extra = np.abs(np.asarray(offset1, np.float16).astype(np.float64)) + \
+                np.abs(np.asarray(scale1, np.float16).astype(np.float64))
+            if mistake == "record coefficients on every group":
+                for j, r in enumerate(rows):
+                    coef[r, :] += extra[j]
+            elif mistake != "records dropped":
+                coef[rows, g] += extra
+        xa = np.abs(np.asarray(X, np.float16).astype(np.float64)).reshape(-1, ng, 128).sum(axis=2)
+        if mistake == "whole-row L1 norm":
+            xa = np.repeat(xa.sum(axis=1, keepdims=True), ng, axis=1)
+        out = (10 * rel if mistake == "rel x 10" else rel) * (xa @ coef.T)
+        return out[0] if np.asarray(X).ndim == 1 else out
+    return bound
+
+
+@pytest.mark.parametrize("mistake", ["rel x 10", "record coefficients on every group", "whole-row L1 norm",
+                                     "records dropped"])
+def test_bound_pins_catch_planted_mistakes(mistake):
+    assert bound_pin_failures(_planted_bound(mistake)), f"no pin failed for: {mistake}"
+
+
+def test_planted_bound_copy_is_faithful():
+    """The copy used for planting, with no mistake, passes every pin."""
+    assert bound_pin_failures(_planted_bound(None)) == []
