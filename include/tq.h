@@ -66,12 +66,14 @@
 extern "C" {
 #endif
 
-#define TQ_ABI_VERSION 5
+#define TQ_ABI_VERSION 6
 #define TQ_GROUP 128
 #define TQ_GROUP_BYTES 26
 #define TQ_MAX_GROUPS_PER_ROW 256    /* K <= 32768 */
 #define TQ_MAX_GROUPED 8             /* matrices per tq_gemv_grouped call */
 #define TQ_MAX_BATCH 64              /* rows of X in tq_gemm_smallbatch */
+#define TQ_SELECT_NOALLOC_MAX_GROUPS (1 << 24)  /* n_out * groups_per_row in
+                                                   tq_select_two_plane_noalloc */
 
 /* Output element type for tq_gemv / tq_gemm_smallbatch (the `flags` word). */
 #define TQ_OUT_FP16 0   /* fp16, rounded to nearest even from fp32 */
@@ -263,6 +265,20 @@ size_t tq_select_workspace_bytes(int64_t n_groups);
 tq_status tq_select_two_plane(const double* energy, int64_t n_out, int32_t groups_per_row, int64_t nnz,
                               int32_t* rec_index, int32_t* rowptr1, uint16_t* gidx1,
                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* tq_select_two_plane without a workspace argument (ABI 6), for callers
+ * that cannot allocate device memory: code under HIP graph capture, serving
+ * loops that must not call hipMalloc, harnesses that forbid it.  Same
+ * arguments (less the workspace), same result bit for bit.  The scratch is
+ * a static array in the library, one per GPU (about 65 KB, held until the
+ * process ends), sized for n_out * groups_per_row <=
+ * TQ_SELECT_NOALLOC_MAX_GROUPS; larger requests return TQ_ERR_UNSUPPORTED
+ * before anything is launched.  The call allocates nothing.  Every call on
+ * one GPU shares that GPU's scratch, so calls that overlap in time on one
+ * GPU (other streams, other host threads) race and give unspecified
+ * results; order them on one stream. */
+tq_status tq_select_two_plane_noalloc(const double* energy, int64_t n_out, int32_t groups_per_row, int64_t nnz,
+                                      int32_t* rec_index, int32_t* rowptr1, uint16_t* gidx1, void* stream);
 
 #ifdef __cplusplus
 }

@@ -24,6 +24,8 @@
 //    rows whose first group lies in the tile.
 // Counts are integers, so the result is deterministic and unique.
 
+#include <mutex>
+
 #include "tq_internal.h"
 
 namespace tq {
@@ -45,7 +47,17 @@ struct SelState {
 constexpr size_t kStateOff = kHistBytes;
 constexpr size_t kTilesOff = kStateOff + sizeof(SelState);
 
-__host__ __device__ inline int64_t num_tiles(int64_t n) { return (n + kTile - 1) / kTile; }
+__host__ __device__ constexpr int64_t num_tiles(int64_t n) { return (n + kTile - 1) / kTile; }
+
+constexpr size_t workspace_bytes_for(int64_t n) {
+  return (kTilesOff + 4 * sizeof(uint32_t) * (size_t)num_tiles(n) + 255) & ~(size_t)255;
+}
+
+// Scratch of the allocation-free entry point: one copy per GPU, held until
+// the process ends.  Host code never passes this name to a kernel; it uses
+// the device address obtained for it below.
+constexpr size_t kScratchBytes = workspace_bytes_for(TQ_SELECT_NOALLOC_MAX_GROUPS);
+static __device__ __attribute__((aligned(256))) unsigned char scratch[kScratchBytes];
 
 // Orderable key of an energy: larger energy, larger key; NaN is 0, below
 // every number (-inf maps to 0x000FFFFFFFFFFFFF); both zeros map to the key
@@ -232,10 +244,7 @@ __global__ void __launch_bounds__(kThreads) sel_write(const double* __restrict__
 
 }  // namespace
 
-size_t select_workspace_bytes(int64_t n) {
-  const size_t b = kTilesOff + 4 * sizeof(uint32_t) * (size_t)num_tiles(n);
-  return (b + 255) & ~(size_t)255;
-}
+size_t select_workspace_bytes(int64_t n) { return workspace_bytes_for(n); }
 
 hipError_t launch_select(const double* energy, int64_t n_out, int32_t G, int64_t nnz, int32_t* rec_index,
                          int32_t* rowptr1, uint16_t* gidx1, void* workspace, hipStream_t s) {
@@ -267,6 +276,37 @@ hipError_t launch_select(const double* energy, int64_t n_out, int32_t G, int64_t
   hipLaunchKernelGGL(sel_write, dim3((unsigned)nt), dim3(kThreads), 0, s, energy, n, G, n_out, nnz, st, eq_off,
                      sel_off, rec_index, rowptr1, gidx);
   return hipGetLastError();
+}
+
+// Device address of `scratch` on the current GPU, looked up once per device
+// (each GPU holds its own copy of the array at its own address).
+static hipError_t scratch_address(void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_select_noalloc(const double* energy, int64_t n_out, int32_t G, int64_t nnz, int32_t* rec_index,
+                                 int32_t* rowptr1, uint16_t* gidx1, hipStream_t s) {
+  if (n_out * G > TQ_SELECT_NOALLOC_MAX_GROUPS) return hipErrorInvalidValue;
+  void* ws = nullptr;
+  const hipError_t e = scratch_address(&ws);
+  if (e != hipSuccess) return e;
+  return launch_select(energy, n_out, G, nnz, rec_index, rowptr1, gidx1, ws, s);
 }
 
 }  // namespace tq

@@ -63,6 +63,21 @@ tq_status check_matrix(const tq_matrix* m, MatDev* d) {
   return TQ_OK;
 }
 
+// Arguments shared by both selection entry points (not the workspace).
+tq_status check_select(const double* energy, int64_t n_out, int32_t G, int64_t nnz, const int32_t* rec_index,
+                       const int32_t* rowptr1, const uint16_t* gidx1) {
+  if (n_out < 1 || G < 1 || G > TQ_MAX_GROUPS_PER_ROW) return TQ_ERR_SHAPE;
+  if (n_out > (int64_t)INT32_MAX / G) return TQ_ERR_SHAPE;
+  const int64_t n = n_out * G;
+  if (nnz < 0 || nnz > n) return TQ_ERR_SHAPE;
+  if (energy == nullptr || rec_index == nullptr || rowptr1 == nullptr) return TQ_ERR_NULL;
+  if (nnz > 0 && gidx1 == nullptr) return TQ_ERR_NULL;
+  if (misaligned(energy, 8) || misaligned(rec_index, 4) || misaligned(rowptr1, 4) ||
+      (gidx1 != nullptr && misaligned(gidx1, 2)))
+    return TQ_ERR_ALIGN;
+  return TQ_OK;
+}
+
 tq_status check_flags(int32_t flags) {
   return (flags == TQ_OUT_FP16 || flags == TQ_OUT_FP32) ? TQ_OK : TQ_ERR_UNSUPPORTED;
 }
@@ -193,18 +208,22 @@ size_t tq_select_workspace_bytes(int64_t n_groups) {
 tq_status tq_select_two_plane(const double* energy, int64_t n_out, int32_t groups_per_row, int64_t nnz,
                               int32_t* rec_index, int32_t* rowptr1, uint16_t* gidx1, void* workspace,
                               size_t workspace_bytes, void* stream) {
-  if (n_out < 1 || groups_per_row < 1 || groups_per_row > TQ_MAX_GROUPS_PER_ROW) return TQ_ERR_SHAPE;
-  if (n_out > (int64_t)INT32_MAX / groups_per_row) return TQ_ERR_SHAPE;
-  const int64_t n = n_out * groups_per_row;
-  if (nnz < 0 || nnz > n) return TQ_ERR_SHAPE;
-  if (energy == nullptr || rec_index == nullptr || rowptr1 == nullptr || workspace == nullptr) return TQ_ERR_NULL;
-  if (nnz > 0 && gidx1 == nullptr) return TQ_ERR_NULL;
-  if (workspace_bytes < tq::select_workspace_bytes(n)) return TQ_ERR_SHAPE;
-  if (misaligned(energy, 8) || misaligned(rec_index, 4) || misaligned(rowptr1, 4) || misaligned(workspace, 256) ||
-      (gidx1 != nullptr && misaligned(gidx1, 2)))
-    return TQ_ERR_ALIGN;
+  tq_status st = check_select(energy, n_out, groups_per_row, nnz, rec_index, rowptr1, gidx1);
+  if (st != TQ_OK) return st;
+  if (workspace == nullptr) return TQ_ERR_NULL;
+  if (workspace_bytes < tq::select_workspace_bytes(n_out * groups_per_row)) return TQ_ERR_SHAPE;
+  if (misaligned(workspace, 256)) return TQ_ERR_ALIGN;
   return from_hip(tq::launch_select(energy, n_out, groups_per_row, nnz, rec_index, rowptr1, gidx1, workspace,
                                     (hipStream_t)stream));
+}
+
+tq_status tq_select_two_plane_noalloc(const double* energy, int64_t n_out, int32_t groups_per_row, int64_t nnz,
+                                      int32_t* rec_index, int32_t* rowptr1, uint16_t* gidx1, void* stream) {
+  tq_status st = check_select(energy, n_out, groups_per_row, nnz, rec_index, rowptr1, gidx1);
+  if (st != TQ_OK) return st;
+  if (n_out * groups_per_row > TQ_SELECT_NOALLOC_MAX_GROUPS) return TQ_ERR_UNSUPPORTED;
+  return from_hip(tq::launch_select_noalloc(energy, n_out, groups_per_row, nnz, rec_index, rowptr1, gidx1,
+                                            (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -62,5 +62,8 @@ hipError_t launch_ternarize(const uint16_t* w, int64_t n_groups, const int32_t* 
 size_t select_workspace_bytes(int64_t n_groups);
 hipError_t launch_select(const double* energy, int64_t n_out, int32_t G, int64_t nnz, int32_t* rec_index,
                          int32_t* rowptr1, uint16_t* gidx1, void* workspace, hipStream_t s);
+// The same with the library's static per-device scratch (no allocation).
+hipError_t launch_select_noalloc(const double* energy, int64_t n_out, int32_t G, int64_t nnz, int32_t* rec_index,
+                                 int32_t* rowptr1, uint16_t* gidx1, hipStream_t s);
 
 }  // namespace tq

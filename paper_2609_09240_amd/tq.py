@@ -16,7 +16,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtq.so")
 
-ABI_VERSION = 5
+ABI_VERSION = 6
 GROUP = 128
 GROUP_BYTES = 26
 OUT_FP16 = 0
@@ -78,6 +78,7 @@ def lib():
             "tq_ternarize": ([vp, i64, i32, vp, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp], ctypes.c_int),
             "tq_select_workspace_bytes": ([i64], ctypes.c_size_t),
             "tq_select_two_plane": ([vp, i64, i32, i64, vp, vp, vp, vp, ctypes.c_size_t, vp], ctypes.c_int),
+            "tq_select_two_plane_noalloc": ([vp, i64, i32, i64, vp, vp, vp, vp], ctypes.c_int),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(L, name)
@@ -365,6 +366,16 @@ def tq_select_two_plane(energy, n_out, groups_per_row, nnz, rec_index=None, rowp
                                      _ptr(gidx1) if nnz else None, _ptr(workspace), workspace.numel(),
                                      _stream(stream)), "tq_select_two_plane")
     _used_on(stream, energy, rec_index, rowptr1, gidx1, workspace)
+    return rec_index, rowptr1, gidx1
+
+
+def tq_select_two_plane_noalloc(energy, n_out, groups_per_row, nnz, rec_index, rowptr1, gidx1, stream=None):
+    """tq_select_two_plane on the library's static scratch: the caller
+    passes every output buffer and nothing is allocated."""
+    _cuda(energy, torch.float64, "energy")
+    _check(lib().tq_select_two_plane_noalloc(_ptr(energy), n_out, groups_per_row, nnz, _ptr(rec_index),
+                                             _ptr(rowptr1), _ptr(gidx1) if nnz else None, _stream(stream)),
+           "tq_select_two_plane_noalloc")
     return rec_index, rowptr1, gidx1
 
 

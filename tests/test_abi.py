@@ -44,7 +44,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert tq.tq_abi_version() == tq.ABI_VERSION == 5
+    assert tq.tq_abi_version() == tq.ABI_VERSION == 6
     for s in range(6):
         assert tq.tq_status_string(s).startswith(tq.STATUS[s])
     assert "unknown" in tq.tq_status_string(42)
