@@ -1,19 +1,20 @@
 """Benchmark: the Qwen3-8B decode-step linear stack as packed ternary GEMVs.
 
 One step = every packed linear of one decode step at batch 1: 36 layers x
-{q, k, v, o, gate, up, down} (252 matrices, 6.95 G weights), run in
-dependency order as 144 launches per step (q+k+v grouped, o, gate+up grouped,
-down), captured once in a HIP graph and replayed.  Inputs are seeded
+{q, k, v, o, gate, up, down} (252 matrices, 6.95 G weights) as 144 dependent
+stages (q+k+v grouped, o, gate+up grouped, down), run as one tq_gemv_chain
+launch per step; the same step as 144 launches in a HIP graph is reported
+beside it (outputs compared bit for bit).  Inputs are seeded
 synthetic stand-ins for the paper's converted weights (shapes of section 3,
 10% two-plane groups) and stay resident in HBM; the 1.70 GB of packed weights
 is far larger than the caches, so every step streams them from HBM.
 
 Prints one JSON line: value = aggregate GB/s of algorithmic bytes (packed
 weights + activations + outputs) per step time, plus ms_per_step, the
-roofline of the GEMV kernel (its average launch duration: the HIP-event
+roofline of chain_kernel (one launch per step: its duration is the HIP-event
 timed region on the launch stream over the launches it holds), the measured
 streaming-read ceiling at the same byte count and the CPU oracle timed on a
-bounded sample.
+bounded sample (all host cores and one thread).
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--layers 36]
     python bench.py --extra     # also: small batch, codec, and the 4096 x 2560
@@ -133,6 +134,47 @@ def time_stack(mats, xs, steps, warmup):
     return ms_per_step, launches, graph, outs
 
 
+def time_chain(mats, xs, steps, warmup):
+    """The same decode step as one tq_gemv_chain launch per step (every
+    stage waits for the previous one inside the launch); HIP events on the
+    launch stream around `steps` calls.  Returns (ms per step, chain,
+    outputs, spread)."""
+    import torch
+
+    from paper_2609_09240_amd import tq
+    launches = step_launches(mats, xs)
+    dev = xs[0][0].device
+    outs = [[torch.empty(m.n_out, dtype=torch.float16, device=dev) for m in ms] for ms, _ in launches]
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        chain = tq.Chain([(ms, x, ys) for (ms, x), ys in zip(launches, outs)], stream=stream)
+        for _ in range(warmup):
+            chain.run(stream=stream)
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_stop = torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        t_start.record(stream)
+        for _ in range(steps):
+            chain.run(stream=stream)
+        t_stop.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t_start.elapsed_time(t_stop) / steps
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    with torch.cuda.stream(stream):
+        for a, b in evs:
+            a.record(stream)
+            chain.run(stream=stream)
+            b.record(stream)
+    torch.cuda.synchronize()
+    per_step = sorted(a.elapsed_time(b) * 1e3 for a, b in evs)
+    spread = [round(per_step[min(len(per_step) - 1, int(q / 100 * len(per_step)))], 2) for q in (10, 50, 90)]
+    err = chain.error_flag()
+    if err:
+        raise RuntimeError("tq_gemv_chain: a stage wait gave up (sync error flag set)")
+    return ms_per_step, chain, outs, spread
+
+
 def algorithmic_bytes(launches):
     total = 0
     for ms, x in launches:
@@ -141,25 +183,43 @@ def algorithmic_bytes(launches):
     return total
 
 
-def measured_traffic():
-    """HBM bytes per GEMV launch from the committed rocprofv3 summary, if it
-    was taken on the current kernel source (else None)."""
+def kernel_source_hash(path):
+    """sha256[:16] of the sources of the step's dominant kernel."""
     import hashlib
+    files = ("chain.hip", "gemv_decode.h") if path == "chain" else ("gemv.hip", "gemv_decode.h")
+    h = hashlib.sha256()
+    for f in files:
+        h.update(open(os.path.join(ROOT, "paper_2609_09240_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(path):
+    """HBM bytes per launch of the step's dominant kernel from the committed
+    rocprofv3 counter summary, if it was taken on the current kernel sources
+    (else None)."""
     import re
-    src = os.path.join(ROOT, "paper_2609_09240_amd", "csrc", "gemv.hip")
-    prof = os.path.join(ROOT, "profiles", "gemv_qwen3_8b_decode_step.md")
+    name = "chain_kernel_qwen3_8b_decode_step.md" if path == "chain" else "gemv_qwen3_8b_decode_step.md"
+    prof = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(prof):
         return None
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    m = re.search(r"traffic_bytes_per_launch = (\d+)\s+\(gemv.hip sha256\[:16\] = ([0-9a-f]+)\)",
+    m = re.search(r"traffic_bytes_per_launch = (\d+)\s+\(sources sha256\[:16\] = ([0-9a-f]+)\)",
                   open(prof).read())
-    return float(m.group(1)) if m and m.group(2) == sha else None
+    return float(m.group(1)) if m and m.group(2) == kernel_source_hash(path) else None
 
 
-def cpu_baseline(layers=2):
-    """The oracle (numpy fp64) on the first `layers` layers of the same stack."""
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_rate(layers):
+    """Algorithmic bytes and seconds of the oracle's gemv over `layers`."""
     import numpy as np
-    from threadpoolctl import threadpool_info
 
     from oracle import accounting, codec, packed
     from paper_2609_09240_amd import synth
@@ -175,11 +235,25 @@ def cpu_baseline(layers=2):
             secs += time.perf_counter() - t
             assert np.all(np.isfinite(y))
             nbytes += accounting.gemv_bytes(inp.n_out, inp.n_in, inp.nnz1)
+    return nbytes, secs
+
+
+def cpu_baseline(layers=2, layers_1t=1):
+    """The oracle (numpy fp64: decode, dequantise, matvec) on the first
+    layers of the same stack, with numpy's BLAS on every host core and then
+    on one thread."""
+    from threadpoolctl import threadpool_info, threadpool_limits
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    nbytes, secs = _oracle_rate(layers)
+    with threadpool_limits(limits=1):
+        nb1, s1 = _oracle_rate(layers_1t)
     return {"value": round(nbytes / secs / 1e9, 6), "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": f"oracle gemv (decode + fp64 dequant + fp64 matvec) of layers 0..{layers - 1} "
-                      f"(7 projections each, {nbytes} algorithmic bytes) in {secs:.1f} s; "
-                      f"host has {os.cpu_count()} logical CPUs"}
+                      f"(7 projections each, {nbytes} algorithmic bytes) in {secs:.1f} s with BLAS on "
+                      f"{threads} threads; host: {os.cpu_count()} logical CPUs, {cpu_model()}",
+            "one_thread": {"value": round(nb1 / s1 / 1e9, 6), "unit": "GB/s", "cores": 1,
+                           "sample": f"layer 0 (7 projections, {nb1} bytes) in {s1:.1f} s"},
+            "cpu_model": cpu_model(), "logical_cpus": os.cpu_count()}
 
 
 def graph_time_us(calls, reps=3):
@@ -397,22 +471,49 @@ def main():
     torch.cuda.set_device(dev)
 
     mats, xs = build_stack(args.layers, dev)
-    ms_per_step, launches, graph, outs = time_stack(mats, xs, args.steps, args.warmup)
+    launches = step_launches(mats, xs)
     step_bytes = algorithmic_bytes(launches)
     weight_bytes = sum(m.nbytes() for ms, _ in launches for m in ms)
     n_weights = sum(m.n_out * m.n_in for ms, _ in launches for m in ms)
-    gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
-    log(f"{args.steps} steps: {ms_per_step * 1e3:.1f} us/step, {gbs:.1f} GB/s")
 
-    # Roofline of the GEMV kernel: its average launch duration is the timed
-    # region (HIP events on the launch stream) divided by the launches it
-    # holds; the graph leaves no host gaps between them.
-    avg_ms = ms_per_step / len(launches)
-    bytes_per_launch = step_bytes / len(launches)
-    achieved = bytes_per_launch / (avg_ms * 1e-3) / 1e9
+    # The step two ways, both timed the same way: one tq_gemv_chain launch
+    # per step, and 144 launches (one per stage) in a HIP graph.  They must
+    # give the same bits; `value` is the faster, named in config.workload.
+    ms_chain, chain, outs_chain, spread_chain = time_chain(mats, xs, args.steps, args.warmup)
+    log(f"chain: {args.steps} steps: {ms_chain * 1e3:.1f} us/step")
+    ms_graph, _, graph, outs_graph = time_stack(mats, xs, args.steps, args.warmup)
+    spread_graph = [time_stack.spread_us[q] for q in (10, 50, 90)]
+    log(f"graph of {len(launches)} launches: {ms_graph * 1e3:.1f} us/step")
+    torch.cuda.synchronize()
+    for a, b in zip(outs_chain, outs_graph):
+        for ya, yb in zip(a, b):
+            if not torch.equal(ya.view(torch.int16), yb.view(torch.int16)):
+                raise RuntimeError("chain and per-launch GEMV outputs differ")
+    del chain, outs_chain, graph, outs_graph
+    torch.cuda.empty_cache()
+    use_chain = ms_chain <= ms_graph
+    ms_per_step = ms_chain if use_chain else ms_graph
+    spread = spread_chain if use_chain else spread_graph
+    gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
+    paths = {
+        "chain": {"us_per_step": round(ms_chain * 1e3, 2), "GBps": round(step_bytes / (ms_chain * 1e-3) / 1e9, 2),
+                  "launches_per_step": 1, "kernel": "chain_kernel",
+                  "what": "tq_gemv_chain: every stage in one cooperative launch"},
+        "graph": {"us_per_step": round(ms_graph * 1e3, 2), "GBps": round(step_bytes / (ms_graph * 1e-3) / 1e9, 2),
+                  "launches_per_step": len(launches), "kernel": "gemv_kernel",
+                  "what": "one tq_gemv / tq_gemv_grouped launch per stage, captured in a HIP graph"},
+    }
+
+    # Roofline of the dominant kernel.  Chain: one launch per step, its
+    # duration is the timed region.  Graph: the timed region over the
+    # launches it holds (an upper bound on the kernel duration: it includes
+    # the gaps between graph nodes).
+    nl = 1 if use_chain else len(launches)
+    avg_ms = ms_per_step / nl
+    achieved = step_bytes / nl / (avg_ms * 1e-3) / 1e9
 
     # Calibration for HBM counters: a plain copy of known size (outside the
-    # timed region), so FETCH_SIZE / WRITE_SIZE of the GEMV can be scaled.
+    # timed region), so FETCH_SIZE / WRITE_SIZE can be scaled.
     cal = torch.empty(COPY_BYTES // 2, dtype=torch.float16, device=dev)
     cal_dst = torch.empty_like(cal)
     for _ in range(3):
@@ -432,10 +533,11 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 6),
         "us_per_step": round(ms_per_step * 1e3, 2),
-        "step_us_p10_p50_p90": [time_stack.spread_us[q] for q in (10, 50, 90)],
+        "step_us_p10_p50_p90": spread,
         "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
         "pct_of_stream_ceiling": round(100 * gbs / ceiling["GBps"], 2),
         "stream_ceiling": ceiling,
+        "step_paths": paths,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -443,9 +545,12 @@ def main():
         "data": "synthetic (seeded; Qwen3-8B projection shapes, 10% two-plane groups)",
         "config": {
             "workload": f"Qwen3-8B decode-step linear stack, batch 1: {args.layers} layers x "
-                        "{q,k,v,o,gate,up,down}, 144 launches per step (q+k+v and gate+up grouped), HIP graph",
+                        "{q,k,v,o,gate,up,down} as 144 dependent stages (q+k+v and gate+up grouped), timed as "
+                        + ("one tq_gemv_chain launch per step" if use_chain else
+                           "144 tq_gemv/tq_gemv_grouped launches per step in a HIP graph"),
+            "step_path": "chain" if use_chain else "graph",
             "layers": args.layers,
-            "launches_per_step": len(launches),
+            "stages_per_step": len(launches),
             "weights_per_step": n_weights,
             "packed_weight_bytes": weight_bytes,
             "algorithmic_bytes_per_step": step_bytes,
@@ -454,14 +559,14 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "gemv_kernel",
+            "kernel": "chain_kernel" if use_chain else "gemv_kernel",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic(),
+            "traffic": measured_traffic("chain" if use_chain else "graph"),
             "avg_launch_us": round(avg_ms * 1e3, 3),
-            "bytes_per_launch": round(bytes_per_launch, 1),
+            "bytes_per_launch": round(step_bytes / nl, 1),
         },
     }
     if not args.no_cpu_baseline:
@@ -469,7 +574,7 @@ def main():
         result["cpu_baseline"] = cpu_baseline()
     print(json.dumps(result), flush=True)
     if args.extra:
-        del graph, outs, launches, mats, xs
+        del launches, mats, xs
         torch.cuda.empty_cache()
         print(json.dumps(paper_representation_line(dev)), flush=True)
         for line in extra_suite(dev):

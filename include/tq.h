@@ -66,7 +66,7 @@
 extern "C" {
 #endif
 
-#define TQ_ABI_VERSION 6
+#define TQ_ABI_VERSION 7
 #define TQ_GROUP 128
 #define TQ_GROUP_BYTES 26
 #define TQ_MAX_GROUPS_PER_ROW 256    /* K <= 32768 */
@@ -279,6 +279,61 @@ tq_status tq_select_two_plane(const double* energy, int64_t n_out, int32_t group
  * results; order them on one stream. */
 tq_status tq_select_two_plane_noalloc(const double* energy, int64_t n_out, int32_t groups_per_row, int64_t nnz,
                                       int32_t* rec_index, int32_t* rowptr1, uint16_t* gidx1, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Decode-step chain (ABI 7): a sequence of dependent grouped GEMVs in one
+ * launch.  Section 13 runs the packed model's whole decode step; within a
+ * decoder layer q, k and v read one input, o the attention output, gate and
+ * up the normalised residual and down the activated MLP state, so at batch
+ * 1 the step is a chain of GEMVs, each waiting for the one before.  Stage s
+ * computes exactly what tq_gemv_grouped(stage s) computes (bit for bit),
+ * and reads its x only after every output of stage s - 1 is written, so x
+ * may be (or be derived by device code in a later design from) an earlier
+ * stage's output.  One cooperative launch of one 1024-thread workgroup per
+ * CU runs every stage; each workgroup keeps the decode table across stages.
+ */
+typedef struct tq_stage {
+  const tq_matrix* mats;   /* host array of n matrices, all with the same n_in */
+  int32_t n;               /* 1 .. TQ_MAX_GROUPED */
+  int32_t flags;           /* TQ_OUT_FP16 or TQ_OUT_FP32 */
+  const uint16_t* x;       /* device fp16 [n_in]; 16-byte aligned */
+  void* const* ys;         /* host array of n device outputs (4-byte aligned) */
+} tq_stage;
+
+typedef struct tq_chain_info {
+  int32_t n_stages;
+  int32_t n_workgroups;    /* one per CU of the device current at planning */
+  int32_t lds_bytes;       /* dynamic LDS per workgroup */
+  int32_t reserved;
+  int64_t plan_bytes;      /* 128 * n_stages * n_workgroups */
+  int64_t sync_bytes;      /* 256 + 64 * n_workgroups */
+} tq_chain_info;
+
+/* Plan a chain for the current device.  Checks every stage (as tq_gemv_
+ * grouped does) and fills *info.  With plan_host != NULL it also writes the
+ * plan, a table of info->plan_bytes bytes of device pointers and row
+ * ranges, into that HOST buffer (plan_host_bytes >= info->plan_bytes); the
+ * caller copies it unchanged to device memory (128-byte aligned) and keeps
+ * every buffer the stages name alive while the plan is used.  Record
+ * ranges come from the matrices' host row pointers where present.  Returns
+ * TQ_ERR_UNSUPPORTED for a stage that does not fit one round of workgroups
+ * (more than 6 row passes per workgroup) or the LDS. */
+tq_status tq_chain_plan(const tq_stage* stages, int32_t n_stages, tq_chain_info* info,
+                        void* plan_host, size_t plan_host_bytes);
+
+/* Zero a sync block (device memory, info->sync_bytes bytes, 256-byte
+ * aligned) on `stream`; required once before its first tq_gemv_chain and
+ * whenever it is reused for a plan with another stage count.  Layout: word
+ * 0 counts completed calls, word 2 (int32 at byte 8) is a sticky error flag
+ * that a call sets when one of its waits gave up (after about 0.1 s; the
+ * outputs of that call are then unspecified), then one 64-byte slot per
+ * workgroup. */
+tq_status tq_chain_sync_init(void* sync, const tq_chain_info* info, void* stream);
+
+/* Run every stage of a planned chain on `stream` (one launch).  `plan` is
+ * the device copy of the plan, `sync` a sync block of this plan.  Calls on
+ * one sync block must not overlap in time. */
+tq_status tq_gemv_chain(const void* plan, void* sync, const tq_chain_info* info, void* stream);
 
 #ifdef __cplusplus
 }

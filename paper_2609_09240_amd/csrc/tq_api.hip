@@ -6,6 +6,9 @@
 
 #include <stdint.h>
 
+#include <memory>
+#include <new>
+
 #include "tq_internal.h"
 
 namespace {
@@ -224,6 +227,92 @@ tq_status tq_select_two_plane_noalloc(const double* energy, int64_t n_out, int32
   if (n_out * groups_per_row > TQ_SELECT_NOALLOC_MAX_GROUPS) return TQ_ERR_UNSUPPORTED;
   return from_hip(tq::launch_select_noalloc(energy, n_out, groups_per_row, nnz, rec_index, rowptr1, gidx1,
                                             (hipStream_t)stream));
+}
+
+tq_status tq_chain_plan(const tq_stage* stages, int32_t n_stages, tq_chain_info* info, void* plan_host,
+                        size_t plan_host_bytes) {
+  if (stages == nullptr || info == nullptr) return TQ_ERR_NULL;
+  if (n_stages < 1) return TQ_ERR_SHAPE;
+  tq::ChainStageDev* st = new (std::nothrow) tq::ChainStageDev[n_stages];
+  if (st == nullptr) return TQ_ERR_SHAPE;
+  std::unique_ptr<tq::ChainStageDev[]> keep(st);
+  tq_status r;
+  for (int s = 0; s < n_stages; ++s) {
+    const tq_stage& S = stages[s];
+    if (S.mats == nullptr || S.ys == nullptr || S.x == nullptr) return TQ_ERR_NULL;
+    if (S.n < 1 || S.n > TQ_MAX_GROUPED) return TQ_ERR_SHAPE;
+    if ((r = check_flags(S.flags)) != TQ_OK) return r;
+    if (misaligned(S.x, 16)) return TQ_ERR_ALIGN;
+    st[s].n = S.n;
+    st[s].out_f32 = S.flags == TQ_OUT_FP32;
+    st[s].x = S.x;
+    for (int i = 0; i < S.n; ++i) {
+      if ((r = check_matrix(&S.mats[i], &st[s].m[i])) != TQ_OK) return r;
+      if (S.mats[i].n_in != S.mats[0].n_in) return TQ_ERR_SHAPE;
+      if (S.ys[i] == nullptr) return TQ_ERR_NULL;
+      if (misaligned(S.ys[i], 4)) return TQ_ERR_ALIGN;
+      st[s].ys[i] = S.ys[i];
+    }
+  }
+  int nwg = 0;
+  if (tq::chain_workgroups(&nwg) != hipSuccess) return TQ_ERR_HIP;
+  for (int s = 0; s < n_stages; ++s) {
+    int rpw, passes, used;
+    if (!tq::plan_stage(st[s].m, st[s].n, nwg, &rpw, &passes, &used)) return TQ_ERR_UNSUPPORTED;
+  }
+  info->n_stages = n_stages;
+  info->n_workgroups = nwg;
+  info->reserved = 0;
+  info->plan_bytes = (int64_t)sizeof(tq::ChainWork) * n_stages * nwg;
+  info->sync_bytes = tq::chain_sync_head_bytes() + (int64_t)tq::chain_flag_stride_bytes() * nwg;
+  // The plan also decides the LDS: fill it into a scratch table when the
+  // caller asks only for the sizes.
+  std::unique_ptr<tq::ChainWork[]> tmp;
+  tq::ChainWork* out = static_cast<tq::ChainWork*>(plan_host);
+  if (out == nullptr) {
+    tmp.reset(new (std::nothrow) tq::ChainWork[(size_t)n_stages * nwg]);
+    if (!tmp) return TQ_ERR_SHAPE;
+    out = tmp.get();
+  } else if (plan_host_bytes < (size_t)info->plan_bytes) {
+    return TQ_ERR_SHAPE;
+  } else if (misaligned(plan_host, 8)) {
+    return TQ_ERR_ALIGN;
+  }
+  int64_t lds = 0;
+  if (tq::chain_plan_fill(st, n_stages, nwg, out, &lds) != hipSuccess) return TQ_ERR_UNSUPPORTED;
+  if (lds > tq::chain_lds_limit()) return TQ_ERR_UNSUPPORTED;
+  info->lds_bytes = (int32_t)((lds + 15) & ~(int64_t)15);
+  return TQ_OK;
+}
+
+static tq_status check_chain_info(const tq_chain_info* info) {
+  if (info == nullptr) return TQ_ERR_NULL;
+  if (info->n_stages < 1 || info->n_workgroups < 1 || info->lds_bytes < 0 ||
+      info->lds_bytes > tq::chain_lds_limit() ||
+      info->plan_bytes != (int64_t)sizeof(tq::ChainWork) * info->n_stages * info->n_workgroups ||
+      info->sync_bytes != tq::chain_sync_head_bytes() + (int64_t)tq::chain_flag_stride_bytes() * info->n_workgroups)
+    return TQ_ERR_SHAPE;
+  return TQ_OK;
+}
+
+tq_status tq_chain_sync_init(void* sync, const tq_chain_info* info, void* stream) {
+  tq_status r = check_chain_info(info);
+  if (r != TQ_OK) return r;
+  if (sync == nullptr) return TQ_ERR_NULL;
+  if (misaligned(sync, 256)) return TQ_ERR_ALIGN;
+  return from_hip(tq::launch_chain_clear(sync, info->sync_bytes, (hipStream_t)stream));
+}
+
+tq_status tq_gemv_chain(const void* plan, void* sync, const tq_chain_info* info, void* stream) {
+  tq_status r = check_chain_info(info);
+  if (r != TQ_OK) return r;
+  if (plan == nullptr || sync == nullptr) return TQ_ERR_NULL;
+  if (misaligned(plan, 128) || misaligned(sync, 256)) return TQ_ERR_ALIGN;
+  int nwg = 0;
+  if (tq::chain_workgroups(&nwg) != hipSuccess) return TQ_ERR_HIP;
+  if (nwg != info->n_workgroups) return TQ_ERR_SHAPE;   // planned for another device
+  return from_hip(tq::launch_chain(static_cast<const tq::ChainWork*>(plan), info->n_stages, info->n_workgroups,
+                                   info->lds_bytes, sync, (hipStream_t)stream));
 }
 
 }  // extern "C"

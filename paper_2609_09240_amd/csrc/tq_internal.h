@@ -66,4 +66,47 @@ hipError_t launch_select(const double* energy, int64_t n_out, int32_t G, int64_t
 hipError_t launch_select_noalloc(const double* energy, int64_t n_out, int32_t G, int64_t nnz, int32_t* rec_index,
                                  int32_t* rowptr1, uint16_t* gidx1, hipStream_t s);
 
+// ---- Decode-step chain (chain.hip).
+// Work of one workgroup in one stage: rows [row_begin, row_end) of one
+// matrix (none when row_end <= row_begin), read by the kernel from the
+// device copy of the plan.
+struct alignas(128) ChainWork {
+  const uint8_t* codes0;
+  const uint16_t* scale0;
+  const int32_t* rowptr1;
+  const uint16_t* gidx1;
+  const uint8_t* codes1;
+  const uint16_t* offset1;
+  const uint16_t* scale1;
+  const uint16_t* offset0;
+  const uint16_t* x;
+  void* y;
+  int32_t n_out;
+  int32_t nnz1;
+  int32_t row_begin;
+  int32_t row_end;
+  int32_t rec_begin;   // records of the rows; -1: from the device row pointers
+  int32_t rec_end;
+  int32_t G;           // groups per row
+  int32_t flags;       // bit 0: fp32 output; bits 8..15: plane-0 passes
+};
+static_assert(sizeof(ChainWork) == 128, "plan record size");
+
+struct ChainStageDev {
+  MatDev m[TQ_MAX_GROUPED];
+  void* ys[TQ_MAX_GROUPED];
+  const uint16_t* x;
+  int n;
+  bool out_f32;
+};
+
+int chain_lds_limit();
+int chain_sync_head_bytes();
+int chain_flag_stride_bytes();
+hipError_t chain_workgroups(int* nwg);
+bool plan_stage(const MatDev* ms, int n, int nwg, int* rows_per_wg, int* passes, int* used);
+hipError_t chain_plan_fill(const ChainStageDev* st, int n_stages, int nwg, ChainWork* plan, int64_t* max_lds);
+hipError_t launch_chain_clear(void* sync, int64_t bytes, hipStream_t s);
+hipError_t launch_chain(const ChainWork* plan, int n_stages, int nwg, int lds_dyn, void* sync, hipStream_t s);
+
 }  // namespace tq

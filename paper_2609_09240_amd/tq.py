@@ -16,7 +16,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtq.so")
 
-ABI_VERSION = 6
+ABI_VERSION = 7
 GROUP = 128
 GROUP_BYTES = 26
 OUT_FP16 = 0
@@ -53,6 +53,27 @@ class TqMatrix(ctypes.Structure):
     ]
 
 
+class TqStage(ctypes.Structure):
+    _fields_ = [
+        ("mats", ctypes.POINTER(TqMatrix)),
+        ("n", ctypes.c_int32),
+        ("flags", ctypes.c_int32),
+        ("x", ctypes.c_void_p),
+        ("ys", ctypes.POINTER(ctypes.c_void_p)),
+    ]
+
+
+class TqChainInfo(ctypes.Structure):
+    _fields_ = [
+        ("n_stages", ctypes.c_int32),
+        ("n_workgroups", ctypes.c_int32),
+        ("lds_bytes", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+        ("plan_bytes", ctypes.c_int64),
+        ("sync_bytes", ctypes.c_int64),
+    ]
+
+
 _lib = None
 
 
@@ -79,6 +100,10 @@ def lib():
             "tq_select_workspace_bytes": ([i64], ctypes.c_size_t),
             "tq_select_two_plane": ([vp, i64, i32, i64, vp, vp, vp, vp, ctypes.c_size_t, vp], ctypes.c_int),
             "tq_select_two_plane_noalloc": ([vp, i64, i32, i64, vp, vp, vp, vp], ctypes.c_int),
+            "tq_chain_plan": ([ctypes.POINTER(TqStage), i32, ctypes.POINTER(TqChainInfo), vp, ctypes.c_size_t],
+                              ctypes.c_int),
+            "tq_chain_sync_init": ([vp, ctypes.POINTER(TqChainInfo), vp], ctypes.c_int),
+            "tq_gemv_chain": ([vp, vp, ctypes.POINTER(TqChainInfo), vp], ctypes.c_int),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(L, name)
@@ -295,6 +320,49 @@ def tq_gemv_grouped(mats, x, ys=None, out_f32=False, stream=None):
     _check(lib().tq_gemv_grouped(arr, n, _ptr(x), yp, OUT_FP32 if out_f32 else OUT_FP16,
                                  _stream(stream)), "tq_gemv_grouped")
     return ys
+
+
+class Chain:
+    """A planned chain of dependent grouped GEMVs (tq_chain_plan) with its
+    device plan and sync block.  ``stages`` is a list of (matrices, x, ys):
+    stage s computes tq_gemv_grouped(matrices, x) into ys and reads x only
+    after stage s - 1 has finished.  Every tensor named here must outlive the
+    chain."""
+
+    def __init__(self, stages, out_f32=False, stream=None):
+        import numpy as np
+        self._keep = []
+        arr = (TqStage * len(stages))()
+        for st, (mats, x, ys) in zip(arr, stages):
+            _cuda(x, torch.float16, "x")
+            m = (TqMatrix * len(mats))(*[mm.struct() for mm in mats])
+            yp = (ctypes.c_void_p * len(ys))(*[y.data_ptr() for y in ys])
+            self._keep += [m, yp, x, list(mats), list(ys)]
+            st.mats = ctypes.cast(m, ctypes.POINTER(TqMatrix))
+            st.n = len(mats)
+            st.flags = OUT_FP32 if out_f32 else OUT_FP16
+            st.x = x.data_ptr()
+            st.ys = ctypes.cast(yp, ctypes.POINTER(ctypes.c_void_p))
+        self.info = TqChainInfo()
+        _check(lib().tq_chain_plan(arr, len(stages), ctypes.byref(self.info), None, 0), "tq_chain_plan")
+        host = np.zeros(self.info.plan_bytes, dtype=np.uint8)
+        _check(lib().tq_chain_plan(arr, len(stages), ctypes.byref(self.info), host.ctypes.data_as(ctypes.c_void_p),
+                                   host.nbytes), "tq_chain_plan")
+        dev = stages[0][1].device
+        self.plan = torch.from_numpy(host).to(dev)
+        self.sync = torch.empty(self.info.sync_bytes, dtype=torch.uint8, device=dev)
+        _check(lib().tq_chain_sync_init(_ptr(self.sync), ctypes.byref(self.info), _stream(stream)),
+               "tq_chain_sync_init")
+
+    def run(self, stream=None):
+        """tq_gemv_chain: every stage, in order, in one launch."""
+        _check(lib().tq_gemv_chain(_ptr(self.plan), _ptr(self.sync), ctypes.byref(self.info), _stream(stream)),
+               "tq_gemv_chain")
+
+    def error_flag(self, stream=None):
+        """The sync block's sticky error word (nonzero after a call whose
+        waits gave up)."""
+        return int(_host_copy(self.sync[8:12], stream).view(torch.int32).item())
 
 
 def tq_gemm_smallbatch(mat, X, Y=None, out_f32=False, stream=None):

@@ -33,7 +33,8 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for want in ["tq_pack", "tq_unpack", "tq_validate", "tq_unpack_fp16", "tq_gemv", "tq_gemv_grouped",
                  "tq_gemm_smallbatch", "tq_ternarize", "tq_status_string", "tq_abi_version",
-                 "tq_select_workspace_bytes", "tq_select_two_plane"]:
+                 "tq_select_workspace_bytes", "tq_select_two_plane", "tq_select_two_plane_noalloc",
+                 "tq_chain_plan", "tq_chain_sync_init", "tq_gemv_chain"]:
         assert want in names
 
 
@@ -44,7 +45,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert tq.tq_abi_version() == tq.ABI_VERSION == 6
+    assert tq.tq_abi_version() == tq.ABI_VERSION == 7
     for s in range(6):
         assert tq.tq_status_string(s).startswith(tq.STATUS[s])
     assert "unknown" in tq.tq_status_string(42)
@@ -200,6 +201,68 @@ def test_select_rejects_bad_arguments():
     assert call(wb=ws - 1) == 2                                       # workspace too small
     assert call(e=v(FAKE + 4)) == 3 and call(rec=v(FAKE + 2)) == 3 and call(rp=v(FAKE + 2)) == 3
     assert call(gi=v(FAKE + 1)) == 3 and call(w=v(FAKE + 128)) == 3
+
+
+def test_chain_structs_match_header(tmp_path):
+    """The ctypes mirrors of tq_stage and tq_chain_info have the C layout."""
+    src = tmp_path / "chain_layout.c"
+    st = [f[0] for f in tq.TqStage._fields_]
+    ci = [f[0] for f in tq.TqChainInfo._fields_]
+    src.write_text('#include <stddef.h>\n#include <stdio.h>\n#include "tq.h"\nint main(void) {\n'
+                   '  printf("stage %zu\\n", sizeof(tq_stage));\n  printf("info %zu\\n", sizeof(tq_chain_info));\n'
+                   + "".join(f'  printf("s_{f} %zu\\n", offsetof(tq_stage, {f}));\n' for f in st)
+                   + "".join(f'  printf("i_{f} %zu\\n", offsetof(tq_chain_info, {f}));\n' for f in ci)
+                   + "  return 0;\n}\n")
+    exe = tmp_path / "chain_layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = dict(line.split() for line in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                       check=True).stdout.splitlines())
+    assert int(out["stage"]) == ctypes.sizeof(tq.TqStage)
+    assert int(out["info"]) == ctypes.sizeof(tq.TqChainInfo)
+    for f in st:
+        assert int(out["s_" + f]) == getattr(tq.TqStage, f).offset, f
+    for f in ci:
+        assert int(out["i_" + f]) == getattr(tq.TqChainInfo, f).offset, f
+
+
+@no_gpu
+def test_chain_calls_reject_bad_arguments():
+    """Argument errors of the chain entry points come back before any HIP
+    call (the planner's matrix checks are tq_gemv_grouped's)."""
+    L = tq.lib()
+    v = ctypes.c_void_p
+    info = tq.TqChainInfo()
+    m = (tq.TqMatrix * 2)(_mat(), _mat(n_in=512))
+    ys = (ctypes.c_void_p * 2)(FAKE, FAKE)
+
+    def stage(n=1, flags=0, x=FAKE + 0x400000, mats=m, yp=ys):
+        s = tq.TqStage()
+        s.mats = ctypes.cast(mats, ctypes.POINTER(tq.TqMatrix)) if mats is not None else None
+        s.n, s.flags, s.x = n, flags, x
+        s.ys = ctypes.cast(yp, ctypes.POINTER(ctypes.c_void_p)) if yp is not None else None
+        return (tq.TqStage * 1)(s)
+
+    assert L.tq_chain_plan(stage(), 0, ctypes.byref(info), None, 0) == 2
+    assert L.tq_chain_plan(None, 1, ctypes.byref(info), None, 0) == 1
+    assert L.tq_chain_plan(stage(), 1, None, None, 0) == 1
+    assert L.tq_chain_plan(stage(n=0), 1, ctypes.byref(info), None, 0) == 2
+    assert L.tq_chain_plan(stage(n=9), 1, ctypes.byref(info), None, 0) == 2
+    assert L.tq_chain_plan(stage(n=2), 1, ctypes.byref(info), None, 0) == 2     # K differs
+    assert L.tq_chain_plan(stage(flags=3), 1, ctypes.byref(info), None, 0) == 4
+    assert L.tq_chain_plan(stage(x=FAKE + 8), 1, ctypes.byref(info), None, 0) == 3
+    assert L.tq_chain_plan(stage(x=0), 1, ctypes.byref(info), None, 0) == 1
+    assert L.tq_chain_plan(stage(yp=None), 1, ctypes.byref(info), None, 0) == 1
+    bad = (tq.TqMatrix * 1)(_mat(group=64))
+    assert L.tq_chain_plan(stage(mats=bad), 1, ctypes.byref(info), None, 0) == 4
+    # a made-up info block is refused by the run and sync calls
+    info.n_stages, info.n_workgroups, info.lds_bytes, info.plan_bytes, info.sync_bytes = 1, 4, 0, 512, 512
+    info.plan_bytes = 100
+    assert L.tq_gemv_chain(v(FAKE), v(FAKE), ctypes.byref(info), None) == 2
+    assert L.tq_chain_sync_init(v(FAKE), ctypes.byref(info), None) == 2
+    info.plan_bytes = 512
+    assert L.tq_gemv_chain(None, v(FAKE), ctypes.byref(info), None) == 1
+    assert L.tq_gemv_chain(v(FAKE + 64), v(FAKE), ctypes.byref(info), None) == 3
+    assert L.tq_chain_sync_init(v(FAKE + 128), ctypes.byref(info), None) == 3
 
 
 def test_binding_refuses_cpu_tensors():

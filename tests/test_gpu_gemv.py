@@ -172,3 +172,38 @@ def test_grouped_mixes_matrices_with_and_without_offsets():
     for c, yg, y1 in zip(cases, ys, singles):
         assert torch.equal(yg.view(torch.int32), y1.view(torch.int32))
         assert_within_bound(yg.cpu().numpy(), c.oracle_gemm(x[None])[0], c.bound(x), "grouped offsets")
+
+
+def _paper_shape(seed):
+    """The paper's microbenchmark shape (section 13.1: one 4096 x 2560
+    linear; orientation unstated, read as out 4096, in 2560: a 520-byte row
+    of codes, not 16-byte aligned), 10% two-plane groups."""
+    inp = synth.linear(4096, 2560, synth.TWO_PLANE, (9, 4096, 2560, seed))
+    x = synth.activations(2560, (9, 4096, 2560, seed + 1), outlier_frac=0.01)
+    return inp, x
+
+
+def test_paper_microbenchmark_shape_4096x2560():
+    inp, x = _paper_shape(0)
+    check(Case(inp), x, "4096x2560 fp16 out")
+    check(Case(inp), x, "4096x2560 fp32 out", out_f32=True)
+
+
+@pytest.mark.parametrize("out_f32", [False, True])
+def test_unpack_then_dense_route_within_bound(out_f32):
+    """The second GPU route (the paper's chunk-unpack + dense GEMV of
+    section 13.1): tq_unpack_fp16 to a dense fp16 W, then torch's fp16
+    matrix-vector product; every output within the same bound, and the
+    dense W bit-exact with the oracle's fp32-order dequantisation."""
+    from oracle import packed
+    inp, x = _paper_shape(2)
+    case = Case(inp)
+    W = tq.tq_unpack_fp16(case.gpu)
+    xd = torch.from_numpy(x).cuda()
+    y = torch.mv(W.float(), xd.float()) if out_f32 else torch.mv(W, xd)
+    torch.cuda.synchronize()
+    w_want = packed.dequantize_fp16(*case.oracle_args())
+    np.testing.assert_array_equal(W.cpu().numpy().view(np.uint16), w_want.view(np.uint16))
+    want = case.oracle_gemm(x[None])[0]
+    r = assert_within_bound(y.cpu().numpy(), want, case.bound(x), f"unpack + torch.mv (fp32={out_f32})")
+    log(f"4096x2560 unpack + dense mv fp32={out_f32}: max err/bound {r:.3g}")
