@@ -25,9 +25,11 @@
 //   so no cache-wide write-back or invalidate is needed (measured on
 //   MI355X: 1.8 us per stage transition this way, 6.8 us with agent-scope
 //   fences).
-// * A workgroup issues all weight loads of its next stage (codes, scales,
-//   offsets, first records, row bounds) before it waits, so the weights
-//   stream in while the flags propagate.
+// * A workgroup issues the loads of its next stage's first two passes,
+//   first records and row bounds before it waits, so they stream in while
+//   the flags propagate; later passes go out after x, each once the pass
+//   two before it is computed (a wave's loads return in order, so every
+//   load issued before x delays x).
 // * Flags carry an epoch, generation * stages + stage + 1, compared modulo
 //   2^32; the last workgroup to finish a call advances the generation, so
 //   no flag is ever reset.  Every wait is bounded: past its limit a
@@ -111,6 +113,26 @@ __device__ inline void store_y_dev(__amdgpu_buffer_rsrc_t yr, int i, float v, bo
     __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, (_Float16)v), yr, 2 * i, 0, kCoherent);
 }
 
+// One plane-0 pass of a lane: its 12 body bytes in one load.
+struct __attribute__((aligned(4))) Body3 {
+  uint32_t a, b, c;
+};
+__device__ inline void load_pass_c(Pass& p, const uint8_t* body0, const uint8_t* tail0, const uint16_t* scale0,
+                                   const uint16_t* offset0, uint32_t f) {
+  const Body3 b = *reinterpret_cast<const Body3*>(body0 + (size_t)(kMainBytes * f));
+  p.w[0] = b.a;
+  p.w[1] = b.b;
+  p.w[2] = b.c;
+  p.w[3] = __builtin_nontemporal_load(tail0 + (size_t)(2 * f));
+  p.sc = __builtin_nontemporal_load(scale0 + (size_t)f);
+  p.mu = __builtin_nontemporal_load(offset0 + (size_t)f);
+}
+
+// Plane-0 passes whose loads are issued before the wait; the rest go out
+// after x, each once the pass two before it is computed (a wave's loads
+// return in order, so loads issued before x delay x).
+constexpr int kChainAhead = 2;
+
 // One stage for one workgroup: issue its loads, wait for the previous
 // stage (wait_e != 0), stage x, decode, write the outputs, publish my_e.
 // The arithmetic is the batch-1 GEMV's, in the same order.
@@ -176,13 +198,15 @@ __device__ __attribute__((always_inline)) inline void run_stage(const ChainWork&
   const bool has_off = W.offset0 != nullptr;
   const uint16_t* off0 = has_off ? W.offset0 : W.scale0;
   Pass buf[kPasses];
-#pragma unroll
-  for (int d = 0; d < kPasses; ++d) {
+  auto issue_pass = [&](int d) {
     const int r = min(row_begin + rl + d * ri, W.row_end - 1);
     uint32_t rg = (uint32_t)r * (uint32_t)G;
     asm volatile("" : "+v"(rg));
-    load_pass<true>(buf[d], body0, tail0, W.scale0, off0, rg + (uint32_t)g);
-  }
+    load_pass_c(buf[d], body0, tail0, W.scale0, off0, rg + (uint32_t)g);
+  };
+  constexpr int kAhead = kPasses < kChainAhead ? kPasses : kChainAhead;
+#pragma unroll
+  for (int d = 0; d < kAhead; ++d) issue_pass(d);
   const int tr = has_rec ? min(tid, nrb - 1) : 0;
   const int rpa = rpb[tr];
   const int rpz = rpb[has_rec ? tr + 1 : 0];
@@ -221,6 +245,7 @@ __device__ __attribute__((always_inline)) inline void run_stage(const ChainWork&
     float v = code_dot(lut, slot, buf[d].w, xr_) * h2f(buf[d].sc);
     v = v + (has_off ? h2f(buf[d].mu) : 0.f) * xsum;
     asm volatile("" : "+v"(v));
+    if (d + kAhead < kPasses) issue_pass(d + kAhead);
     v = (active && row < nrb) ? v : 0.f;
     const float sum = segment_sum(v, seg);
     if (in_rows && row < nrb && (sl & (seg - 1)) == seg - 1) rowsum[row * segs + (sl >> 6)] = sum;
