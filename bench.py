@@ -316,6 +316,90 @@ def paper_representation_line(dev, layers=36, steps=10, warmup=3):
     return line
 
 
+def per_stage(mats, xs, reps=20):
+    """Each stage kind of the step (q+k+v, o, gate+up, down) timed on its
+    own: a HIP graph of its 36 launches (one per layer, each on that layer's
+    weights, so they stream from HBM), replayed; HIP events on the replay
+    stream.  Per launch: the timed region over the launches it holds (it
+    includes the gap between graph nodes, so it bounds the kernel duration
+    from above).  The four sum to about the per-launch step."""
+    import torch
+
+    from paper_2609_09240_amd import synth, tq
+    out = {}
+    for s, names in enumerate(synth.STAGES):
+        launches = [([mats[layer][n] for n in names], xs[layer][s]) for layer in range(len(mats))]
+        ys = [[torch.empty(m.n_out, dtype=torch.float16, device=xs[0][0].device) for m in ms] for ms, _ in launches]
+        calls = []
+        for (ms, x), y in zip(launches, ys):
+            if len(ms) == 1:
+                calls.append(lambda ms=ms, x=x, y=y: tq.tq_gemv(ms[0], x, y=y[0], stream=torch.cuda.current_stream()))
+            else:
+                calls.append(lambda ms=ms, x=x, y=y: tq.tq_gemv_grouped(ms, x, ys=y, stream=torch.cuda.current_stream()))
+        us = graph_time_us(calls, reps=reps)
+        nbytes = sum(m.nbytes() + 2 * m.n_in + 2 * m.n_out for m in launches[0][0])
+        out["+".join(names)] = {"us_per_launch": round(us, 3), "bytes_per_launch": nbytes,
+                                "GBps": round(nbytes / us / 1e3, 1), "frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4)}
+    return out
+
+
+def config_suite(dev, min_bytes=1 << 30, reps=5):
+    """Single launches of each BASELINE-style configuration, rotating over
+    enough distinct copies (>= 1 GiB) that every call streams its weights
+    from HBM: the 1024 x 4096 one-plane linear, q/k/v/o, gate/up/down (MLP
+    inputs with outlier channels), and tq_unpack_fp16 over the full 36-layer
+    projection set.  Per call: HIP-event graph time over the calls (gaps
+    included; rocprofv3 gives the kernel durations)."""
+    import torch
+
+    from paper_2609_09240_amd import synth, tq
+    lines = []
+    cases = [("cfg0 single linear 1024x4096", synth.single_linear()[0], synth.single_linear()[1])]
+    for name in ("q", "k", "v", "o", "gate", "up", "down"):
+        cfg = 1 if name in ("q", "k", "v", "o") else 2
+        cases.append((f"cfg{cfg} {name}", synth.projection(name, layer=0, cfg=cfg),
+                      synth.stage_activations(synth.STAGE_OF[name], layer=0, cfg=cfg)))
+    for label, inp, x in cases:
+        base = tq.PackedLinear.from_inputs(inp, dev)
+        n = max(2, -(-min_bytes // base.nbytes()))
+        mats = copies_of(base, n)
+        xd = torch.from_numpy(x).to(dev)
+        y = torch.empty(inp.n_out, dtype=torch.float16, device=dev)
+        us = graph_time_us([lambda m=m: tq.tq_gemv(m, xd, y=y, stream=torch.cuda.current_stream()) for m in mats],
+                           reps=reps)
+        nbytes = base.nbytes() + 2 * inp.n_in + 2 * inp.n_out
+        lines.append({"bench": "config_cold", "config": label, "shape": f"{inp.n_out}x{inp.n_in}",
+                      "two_plane_groups": inp.nnz1, "copies": n, "us_per_call": round(us, 3),
+                      "bytes": nbytes, "GBps": round(nbytes / us / 1e3, 1),
+                      "frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4)})
+        del mats, base
+        torch.cuda.empty_cache()
+    # cfg4: tq_unpack_fp16 of every projection of the 36-layer stack, in
+    # order, each into its own output (13.9 GB written, 1.7 GB read: both
+    # far beyond the caches).
+    mats, _ = build_stack(36, dev)
+    seq = [m for layer in mats for m in layer.values()]
+    outs = [torch.empty(m.n_out, m.n_in, dtype=torch.float16, device=dev) for m in seq]
+    for m, w in zip(seq[:7], outs[:7]):
+        tq.tq_unpack_fp16(m, w=w)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for m, w in zip(seq, outs):
+        tq.tq_unpack_fp16(m, w=w)
+    b.record()
+    torch.cuda.synchronize()
+    t_total = a.elapsed_time(b) * 1e3
+    nbytes = sum(m.nbytes() + 2 * m.n_out * m.n_in for m in seq)
+    nw = sum(m.n_out * m.n_in for m in seq)
+    lines.append({"bench": "config_cold", "config": "cfg4 tq_unpack_fp16, 36-layer set (252 matrices)",
+                  "weights": nw, "us_total": round(t_total, 1), "bytes": nbytes,
+                  "GBps": round(nbytes / t_total / 1e3, 1), "frac": round(nbytes / t_total / 1e3 / HBM_PEAK_GBS, 4)})
+    del outs, seq, mats
+    torch.cuda.empty_cache()
+    return lines
+
+
 def extra_suite(dev):
     """Small batch (MFMA path), codec throughput, and the paper's 4096 x 2560
     comparison (dense fp16 GEMV, packed GEMV, unpack + dense GEMV)."""
@@ -454,6 +538,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--layers", type=int, default=36)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--configs", action="store_true",
+                    help="also print one cold-cache line per configuration (single launches over >= 1 GiB of copies)")
     ap.add_argument("--extra", action="store_true",
                     help="also print small-batch, codec and 4096 x 2560 comparison lines")
     args = ap.parse_args()
@@ -491,6 +577,8 @@ def main():
                 raise RuntimeError("chain and per-launch GEMV outputs differ")
     del chain, outs_chain, graph, outs_graph
     torch.cuda.empty_cache()
+    stages = per_stage(mats, xs)
+    log("per stage: " + ", ".join(f"{k} {v['us_per_launch']} us" for k, v in stages.items()))
     use_chain = ms_chain <= ms_graph
     ms_per_step = ms_chain if use_chain else ms_graph
     spread = spread_chain if use_chain else spread_graph
@@ -567,15 +655,21 @@ def main():
             "traffic": measured_traffic("chain" if use_chain else "graph"),
             "avg_launch_us": round(avg_ms * 1e3, 3),
             "bytes_per_launch": round(step_bytes / nl, 1),
+            "per_stage": stages,
+            "dominant": max(stages, key=lambda k: stages[k]["us_per_launch"]),
         },
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample ...")
         result["cpu_baseline"] = cpu_baseline()
     print(json.dumps(result), flush=True)
-    if args.extra:
+    if args.configs or args.extra:
         del launches, mats, xs
         torch.cuda.empty_cache()
+    if args.configs:
+        for line in config_suite(dev):
+            print(json.dumps(line), flush=True)
+    if args.extra:
         print(json.dumps(paper_representation_line(dev)), flush=True)
         for line in extra_suite(dev):
             print(json.dumps(line), flush=True)
