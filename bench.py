@@ -256,9 +256,11 @@ def cpu_baseline(layers=2, layers_1t=1):
             "cpu_model": cpu_model(), "logical_cpus": os.cpu_count()}
 
 
-def graph_time_us(calls, reps=3):
-    """Median over `reps` replays of a HIP graph holding `calls` (a list of
-    zero-argument launches), per call, in microseconds."""
+def graph_time_us(calls, reps=3, back_to_back=1):
+    """Median over `reps` timed regions of a HIP graph holding `calls` (a
+    list of zero-argument launches), per call, in microseconds.  Each timed
+    region replays the graph `back_to_back` times between one pair of
+    events, as the decode step's timed region does."""
     import torch
     stream = torch.cuda.Stream()
     with torch.cuda.stream(stream):
@@ -275,10 +277,11 @@ def graph_time_us(calls, reps=3):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         with torch.cuda.stream(stream):
             a.record(stream)
-            g.replay()
+            for _ in range(back_to_back):
+                g.replay()
             b.record(stream)
         torch.cuda.synchronize()
-        times.append(a.elapsed_time(b) * 1e3 / len(calls))
+        times.append(a.elapsed_time(b) * 1e3 / (len(calls) * back_to_back))
     return sorted(times[1:])[reps // 2]
 
 
@@ -316,13 +319,14 @@ def paper_representation_line(dev, layers=36, steps=10, warmup=3):
     return line
 
 
-def per_stage(mats, xs, reps=20):
+def per_stage(mats, xs, reps=5, back_to_back=10):
     """Each stage kind of the step (q+k+v, o, gate+up, down) timed on its
     own: a HIP graph of its 36 launches (one per layer, each on that layer's
-    weights, so they stream from HBM), replayed; HIP events on the replay
-    stream.  Per launch: the timed region over the launches it holds (it
-    includes the gap between graph nodes, so it bounds the kernel duration
-    from above).  The four sum to about the per-launch step."""
+    weights, so they stream from HBM), replayed 10 times back to back
+    between one pair of HIP events on the replay stream (as the step is
+    timed), median of 5.  Per launch: the timed region over the launches it
+    holds (it includes the gap between graph nodes, so it bounds the kernel
+    duration from above)."""
     import torch
 
     from paper_2609_09240_amd import synth, tq
@@ -336,7 +340,7 @@ def per_stage(mats, xs, reps=20):
                 calls.append(lambda ms=ms, x=x, y=y: tq.tq_gemv(ms[0], x, y=y[0], stream=torch.cuda.current_stream()))
             else:
                 calls.append(lambda ms=ms, x=x, y=y: tq.tq_gemv_grouped(ms, x, ys=y, stream=torch.cuda.current_stream()))
-        us = graph_time_us(calls, reps=reps)
+        us = graph_time_us(calls, reps=reps, back_to_back=back_to_back)
         nbytes = sum(m.nbytes() + 2 * m.n_in + 2 * m.n_out for m in launches[0][0])
         out["+".join(names)] = {"us_per_launch": round(us, 3), "bytes_per_launch": nbytes,
                                 "GBps": round(nbytes / us / 1e3, 1), "frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4)}

@@ -68,40 +68,13 @@ namespace {
 
 #include "gemv_decode.h"
 
-// Record-range table entries passed with a launch (host ranges).
-constexpr int kMaxRangeEntries = 768;
+#include "gemv_args.h"
+
 // Plane-0 passes whose loads are issued before the set-up.
 constexpr int kPrefetch = 2;
 // Most record sweeps a record wave may take (more sweeps measured slower:
 // the record waves then compete with plane 0 for the LDS).
 constexpr int kMaxRecSweeps = 1;
-
-// ---------------------------------------------------------------- params
-// Per-matrix launch record, read by the kernel straight from the kernel-
-// argument segment.
-struct GemvMat {
-  const uint8_t* codes0;
-  const uint16_t* scale0;
-  const int32_t* rowptr1;
-  const uint16_t* gidx1;
-  const uint8_t* codes1;
-  const uint16_t* offset1;
-  const uint16_t* scale1;
-  const uint16_t* offset0;   // per-group offsets on every group, or NULL
-  void* y;
-  int32_t n_out;
-  int32_t nnz1;       // < 2^31: the host caps code buffers at 2^32 bytes
-  int32_t wg_begin;   // first workgroup of this matrix
-  int32_t pad;
-};
-struct GemvArgs {
-  GemvMat m[TQ_MAX_GROUPED];
-  // With host ranges: the first record of every workgroup, matrix by
-  // matrix, each matrix closed by its nnz1 (entry of workgroup w of matrix
-  // i is rec_begin[w + i]).
-  int32_t rec_begin[kMaxRangeEntries];
-};
-
 
 // kPasses: plane-0 passes per lane (the first kPrefetch loaded before the
 // set-up).  kXLoads: 16-byte
