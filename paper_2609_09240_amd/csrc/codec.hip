@@ -12,8 +12,9 @@
 // loads and stores and consecutive lanes touch consecutive memory.  A trit
 // buffer that is not 16-byte aligned takes a one-byte-per-thread kernel.
 // Validate reads the code buffer in flat 16-byte chunks.  The fp16
-// dequantisation stages one row's codes, scales and plane-1 record table in
-// LDS and writes the row with 16-byte stores.
+// dequantisation stages blocks of rows in LDS with coalesced loads, gives
+// each thread 8-weight items and writes them with 16-byte nontemporal stores;
+// persistent workgroups load the next block while storing the current one.
 
 #include <type_traits>
 
@@ -30,8 +31,6 @@ constexpr int kPartMaxBlocks = 2048;
 
 constexpr int kByteThreads = 256;
 
-constexpr int kRowThreads = 64;     // fp16 dequantisation: one row per workgroup pass
-constexpr int kRowMaxBlocks = 8192;
 
 inline int64_t clamp_blocks(int64_t b, int64_t cap) { return b < 1 ? 1 : (b > cap ? cap : b); }
 
@@ -360,173 +359,241 @@ __device__ inline uint32_t pair_selector(int e) {
   return sel[e & 3] | (sel[(e >> 2) & 3] << 16);
 }
 
-// One wave per workgroup, so the LDS writes of a row (table reset, record
-// scatter) take effect in program order without barriers between them.
-// Dynamic LDS, 72 bytes per group of the row:
-//   grp_s  [8 G] words: per group bytes 0..23, 24..25, six zero bytes
-//   rcd_s  [8 G] words: the same for the row's plane-1 records (slot q =
-//          record k - rowptr1[r]), with mu | s1 << 16 in the last word
-//   rec_s  [G]   record slot of each group, or -1
-//   scale_s[G]   s0
-//   off_s  [G]   mu0 (per-group offsets; unused without them)
-constexpr int kCodeBatch = 12;   // code words loaded per thread before one wait (6 G <= 768 in one batch)
-constexpr int kGroupBatch = 4;   // G <= 256 tails and scales per thread in one batch
+// Work split: a workgroup of 256 threads takes a block of RB whole rows
+// (ng = RB * G <= 256 groups) and every thread owns 8-weight items of it
+// (16 output bytes; 16 lanes per group, so a wave's store covers 1 KiB of
+// consecutive output).  The block's plane-0 bytes arrive with coalesced dword
+// loads and are staged in LDS, 8 words per group: bytes 0..23, the two tail
+// bytes, and s0 | mu0 << 16.  Thread q of the block loads the block's q-th
+// plane-1 record (rows' records are consecutive in the CSR arrays) into an
+// LDS slot and points the group's entry of a map at it.
+//
+// Workgroups are persistent (a few per CU) and pipelined: while a block is
+// decoded and stored, the loads of the next block (plane-0 words, records)
+// and the row pointers of the one after are already in flight.  They are all
+// issued before the current block's stores, and every load is unconditional
+// (clamped to valid addresses), so waiting for them never waits for a store.
+// With kExact every thread stores exactly kItems items per block (the host
+// picks RB and kItems so that 16 * RB * G = 256 * kItems and RB divides N);
+// the general variant bounds-checks its items instead.
+constexpr int kDqThreads = 256;
+constexpr int kDqMaxRows = 8;        // rows per block (small G)
+constexpr int kDqBlocksPerCU = 4;    // persistent workgroups per CU
+constexpr int kDqGeneralItems = 8;   // items per thread per pass, general variant
 
-__global__ void __launch_bounds__(kRowThreads) unpack_fp16_kernel(MatDev m, uint16_t* __restrict__ w) {
-  static_assert(kRowThreads == 64, "the row staging relies on a one-wave workgroup");
+__host__ __device__ constexpr int dq_general_rows(int G) {
+  return 16 * G >= kDqThreads * kDqGeneralItems
+             ? 1
+             : (kDqThreads * kDqGeneralItems / (16 * G) < kDqMaxRows ? kDqThreads * kDqGeneralItems / (16 * G)
+                                                                      : kDqMaxRows);
+}
+
+template <bool kRec, bool kOff, int kItems, bool kExact>
+__global__ void __launch_bounds__(kDqThreads) unpack_fp16_kernel(MatDev m, uint16_t* __restrict__ w, int RB) {
+  static_assert(kDqThreads == 256 && kDqThreads >= TQ_MAX_GROUPS_PER_ROW,
+                "one digit-table entry per thread; a block's groups and records fit one per thread");
   __shared__ uint32_t digits[256];
   __shared__ uint32_t selector[16];
-  extern __shared__ uint32_t dyn[];
+  __shared__ int32_t rec_s[2][TQ_MAX_GROUPS_PER_ROW];            // group -> record slot, or -1 (two blocks)
+  __shared__ uint32_t grp_s[8 * TQ_MAX_GROUPS_PER_ROW];          // staged plane-0 words
+  __shared__ uint32_t rcd_s[kRec ? 8 * TQ_MAX_GROUPS_PER_ROW : 8];   // staged records: 6 code words, tail, mu | s1 << 16
+  constexpr int kBlockItems = kDqThreads * kItems;
   const int G = m.n_groups;
-  uint32_t* grp_s = dyn;
-  uint32_t* rcd_s = dyn + 8 * G;
-  int32_t* rec_s = reinterpret_cast<int32_t*>(dyn + 16 * G);
-  uint16_t* scale_s = reinterpret_cast<uint16_t*>(rec_s + G);
-  uint16_t* off_s = scale_s + G;
-  const bool has_off = m.offset0 != nullptr;
-  const uint16_t* off_src = has_off ? m.offset0 : m.scale0;   // without offsets: a readable stand-in
   const int tid = threadIdx.x;
-  for (int c = tid; c < 256; c += kRowThreads) digits[c] = digit_fields(c);
-  if (tid < 16) selector[tid] = pair_selector(tid);
   const int64_t n = (int64_t)m.n_out * G;
-  for (int r = blockIdx.x; r < m.n_out; r += gridDim.x) {
-    const int64_t f0 = (int64_t)r * G;
-    int k0 = 0, R = 0;
-    if (m.nnz1 > 0) {
-      k0 = m.rowptr1[r];
-      R = m.rowptr1[r + 1] - k0;
-      R = R < G ? R : G;   // a valid row has at most G records
+  const int64_t n_blocks = ((int64_t)m.n_out + RB - 1) / RB;
+  const uint32_t* c0 = reinterpret_cast<const uint32_t*>(m.codes0);
+  const uint16_t* t0 = reinterpret_cast<const uint16_t*>(m.codes0 + (int64_t)kMainBytes * n);
+  const uint32_t* c1 = reinterpret_cast<const uint32_t*>(m.codes1);
+  const uint16_t* t1 = reinterpret_cast<const uint16_t*>(m.codes1 + (int64_t)kMainBytes * m.nnz1);
+  const int64_t kmax = m.nnz1 > 0 ? m.nnz1 - 1 : 0;
+  const int64_t b0 = blockIdx.x, gs = gridDim.x;
+  if (b0 >= n_blocks) return;
+  digits[tid] = digit_fields(tid);
+  if (tid < 16) selector[tid] = pair_selector(tid);
+
+  // Registers of the block being staged.
+  uint32_t mw[6], tl, sc, mo;   // plane-0: 6 main words, tail, s0, mu0
+  uint32_t rv[8];               // this thread's record: 6 code words, tail, mu | s1 << 16
+  int rg = G, rslot = 0;        // its group in the row (G: none) and slot
+  int rpv = 0;                  // lane j < 16: rowptr1[r0 + min(j, nr)]
+  auto rows = [&](int64_t b, int& r0, int& nr) {
+    b = b < n_blocks ? b : n_blocks - 1;   // past the end: the last block again (loads only)
+    r0 = (int)(b * RB);
+    nr = m.n_out - r0 < RB ? m.n_out - r0 : RB;
+  };
+  auto load_plane0 = [&](int64_t b) {
+    int r0, nr;
+    rows(b, r0, nr);
+    const int ng = nr * G;
+    const int64_t f0 = (int64_t)r0 * G;
+#pragma unroll
+    for (int u = 0; u < 6; ++u) {
+      int i = u * kDqThreads + tid;
+      i = i < 6 * ng ? i : 6 * ng - 1;
+      mw[u] = c0[6 * f0 + i];
     }
-    // Plane-0 bytes of the row: 6 G words from 24 f0, then 2 G tail bytes.
-    const uint32_t* src = reinterpret_cast<const uint32_t*>(m.codes0 + 24 * f0);
-    const uint16_t* tsrc = reinterpret_cast<const uint16_t*>(m.codes0 + (int64_t)kMainBytes * n) + f0;
-    uint32_t tl[kGroupBatch], sc[kGroupBatch], mo[kGroupBatch];
+    const int gt = tid < ng ? tid : ng - 1;
+    tl = t0[f0 + gt];
+    sc = m.scale0[f0 + gt];
+    mo = kOff ? m.offset0[f0 + gt] : 0u;
+  };
+  auto load_rowptr = [&](int64_t b) {
+    int r0, nr;
+    rows(b, r0, nr);
+    const int j = (tid & 15) < nr ? (tid & 15) : nr;
+    rpv = m.rowptr1[r0 + j];
+  };
+  auto load_records = [&](int64_t b) {   // rpv holds block b's row pointers
+    int r0, nr;
+    rows(b, r0, nr);
+    int rp[kDqMaxRows + 1];
 #pragma unroll
-    for (int u = 0; u < kGroupBatch; ++u) {
-      const int g = tid + u * kRowThreads;
-      tl[u] = g < G ? tsrc[g] : 0u;
-      sc[u] = g < G ? m.scale0[f0 + g] : 0u;
-      mo[u] = g < G ? off_src[f0 + g] : 0u;
+    for (int j = 0; j <= kDqMaxRows; ++j) rp[j] = __builtin_amdgcn_readlane(rpv, j);
+    // Record k = rp[0] + tid lies in row rr (rp[rr] <= k < rp[rr + 1]) at
+    // position q; a row keeps at most G records, and k stays in [0, nnz1).
+    const int k = rp[0] + tid;
+    int rr = 0, lo_k = rp[0], hi_k = rp[1];
+#pragma unroll
+    for (int j = 1; j < kDqMaxRows; ++j)
+      if (j < nr && rp[j] <= k) {
+        rr = j;
+        lo_k = rp[j];
+        hi_k = rp[j + 1];
+      }
+    const int q = k - lo_k;
+    const bool have = k >= 0 && k < m.nnz1 && k < hi_k && q >= 0 && q < G;
+    const int64_t kc = have ? k : kmax;
+    const int gi = m.gidx1[kc];
+#pragma unroll
+    for (int e = 0; e < 6; ++e) rv[e] = c1[6 * kc + e];
+    rv[6] = t1[kc];
+    rv[7] = (uint32_t)m.offset1[kc] | ((uint32_t)m.scale1[kc] << 16);
+    rg = have ? gi : G;
+    rslot = rr * G + q;
+  };
+  auto clear_map = [&](int64_t b, int par) {
+    int r0, nr;
+    rows(b, r0, nr);
+    if (tid < nr * G) rec_s[par][tid] = -1;
+  };
+
+  auto step = [&](int64_t b, int par) {
+    int r0, nr;
+    rows(b, r0, nr);
+    const int ng = nr * G;
+    const int64_t f0 = (int64_t)r0 * G;
+    // Stage block b from registers.
+#pragma unroll
+    for (int u = 0; u < 6; ++u) {
+      const int i = u * kDqThreads + tid;
+      if (i < 6 * ng) grp_s[8 * (i / 6) + i % 6] = mw[u];
     }
-    for (int i0 = 0; i0 < 6 * G; i0 += kCodeBatch * kRowThreads) {
-      uint32_t v[kCodeBatch];
-#pragma unroll
-      for (int u = 0; u < kCodeBatch; ++u) {
-        const int i = i0 + u * kRowThreads + tid;
-        v[u] = i < 6 * G ? src[i] : 0u;
-      }
-#pragma unroll
-      for (int u = 0; u < kCodeBatch; ++u) {
-        const int i = i0 + u * kRowThreads + tid;
-        if (i < 6 * G) grp_s[8 * (i / 6) + i % 6] = v[u];
-      }
+    if (tid < ng) {
+      grp_s[8 * tid + 6] = tl;
+      grp_s[8 * tid + 7] = sc | (mo << 16);
     }
+    if (kRec && rg < G) {
 #pragma unroll
-    for (int u = 0; u < kGroupBatch; ++u) {
-      const int g = tid + u * kRowThreads;
-      if (g < G) {
-        grp_s[8 * g + 6] = tl[u];
-        grp_s[8 * g + 7] = 0u;
-        scale_s[g] = (uint16_t)sc[u];
-        off_s[g] = (uint16_t)mo[u];
-        rec_s[g] = -1;
-      }
+      for (int e = 0; e < 8; ++e) rcd_s[8 * rslot + e] = rv[e];
+      rec_s[par][rslot - rslot % G + rg] = rslot;
     }
-    if (R > 0) {
-      // The row's records: 6 R code words from 24 k0, then per record its tail
-      // bytes, group index, mu and s1.
-      const uint32_t* rsrc = reinterpret_cast<const uint32_t*>(m.codes1 + 24 * (int64_t)k0);
-      const uint16_t* rtail = reinterpret_cast<const uint16_t*>(m.codes1 + (int64_t)kMainBytes * m.nnz1) + k0;
-      for (int i0 = 0; i0 < 6 * R; i0 += kCodeBatch * kRowThreads) {
-        uint32_t v[kCodeBatch];
-#pragma unroll
-        for (int u = 0; u < kCodeBatch; ++u) {
-          const int i = i0 + u * kRowThreads + tid;
-          v[u] = i < 6 * R ? rsrc[i] : 0u;
-        }
-#pragma unroll
-        for (int u = 0; u < kCodeBatch; ++u) {
-          const int i = i0 + u * kRowThreads + tid;
-          if (i < 6 * R) rcd_s[8 * (i / 6) + i % 6] = v[u];
-        }
-      }
-      uint32_t rt[kGroupBatch], ms[kGroupBatch];
-      int gi[kGroupBatch];
-#pragma unroll
-      for (int u = 0; u < kGroupBatch; ++u) {
-        const int q = tid + u * kRowThreads;
-        const bool in = q < R;
-        rt[u] = in ? rtail[q] : 0u;
-        ms[u] = in ? ((uint32_t)m.offset1[k0 + q] | ((uint32_t)m.scale1[k0 + q] << 16)) : 0u;
-        gi[u] = in ? (int)m.gidx1[k0 + q] : G;
-      }
-#pragma unroll
-      for (int u = 0; u < kGroupBatch; ++u) {
-        const int q = tid + u * kRowThreads;
-        if (q < R) {
-          rcd_s[8 * q + 6] = rt[u];
-          rcd_s[8 * q + 7] = ms[u];
-          if (gi[u] < G) rec_s[gi[u]] = q;
-        }
-      }
+    // The next block's loads and the row pointers of the one after.
+    if (kRec) load_records(b + gs);
+    load_plane0(b + gs);
+    if (kRec) {
+      load_rowptr(b + 2 * gs);
+      clear_map(b + gs, par ^ 1);
     }
     __syncthreads();
-    for (int item = tid; item < 16 * G; item += kRowThreads) {
-      const int g = item >> 4;
-      const int p0 = 8 * (item & 15);    // first of the 8 weights
-      const int j0 = p0 / 5, d0 = p0 - 5 * j0;
-      // Code bytes j0..j0+2 (past byte 25 they read 0; those digits are unused).
-      const uint32_t* gw = grp_s + 8 * g + (j0 >> 2);
-      const uint64_t win = (uint64_t)gw[0] | ((uint64_t)gw[1] << 32);
-      const uint32_t bytes = (uint32_t)(win >> (8 * (j0 & 3)));
-      uint32_t D0 = digits[bytes & 0xFFu] | (digits[(bytes >> 8) & 0xFFu] << 10) |
-                    (digits[(bytes >> 16) & 0xFFu] << 20);
-      D0 >>= 2 * d0;   // digit e of the 8 weights at bits 2e, 2e+1
-      const uint32_t s0 = scale_s[g];
-      const int k = rec_s[g];
-      uint32_t o[4];
-      if (!has_off && k < 0 && (s0 & 0x7FFFu) != 0 && (s0 & 0x7C00u) != 0x7C00u) {
-        // One plane, finite nonzero scale: +0 + s0*t is exactly +0 or +-s0.
-        const uint32_t S = s0 | ((s0 ^ 0x8000u) << 16);
+    const int n_items = 16 * ng;
+    auto pass = [&](const int it0) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) o[i] = __builtin_amdgcn_perm(S, S, selector[(D0 >> (4 * i)) & 15u]);
-      } else {
-        // a = +0; a += mu0; a += mu; a += s0*t0; a += s1*t1 in fp32 (each
-        // product exact), rounded once.
-        const float s0f = half_bits_to_float(s0);
-        const float mu0 = half_bits_to_float(off_s[g]);
-        float mu = 0.0f, s1f = 0.0f;
-        uint32_t D1 = 0;
-        if (k >= 0) {
-          const uint32_t* rw = rcd_s + 8 * k;
-          mu = half_bits_to_float(rw[7] & 0xFFFFu);
-          s1f = half_bits_to_float(rw[7] >> 16);
-          const uint64_t rwin = (uint64_t)rw[j0 >> 2] | ((uint64_t)rw[(j0 >> 2) + 1] << 32);
-          const uint32_t rb = (uint32_t)(rwin >> (8 * (j0 & 3)));
-          // bytes past 25 come from the mu|s1 word here; their digits are unused
-          D1 = digits[rb & 0xFFu] | (digits[(rb >> 8) & 0xFFu] << 10) | (digits[(rb >> 16) & 0xFFu] << 20);
-          D1 >>= 2 * d0;
-        }
-        uint32_t h[8];
+      for (int u = 0; u < kItems; ++u) {
+        const int item = it0 + u * kDqThreads + tid;
+        if (!kExact && item >= n_items) break;
+        const int gl = item >> 4, i = item & 15;
+        const int p0 = 8 * i;   // first of the 8 weights
+        const int j0 = p0 / 5, d0 = p0 - 5 * j0;
+        const int wb = j0 >> 2;
+        // Code bytes j0..j0+2 of the group (for j0 = 24: the tail word; bytes
+        // past 25 are zero or the next word's and their digits are unused).
+        const uint32_t* gw = grp_s + 8 * gl;
+        const uint32_t bytes = (uint32_t)((((uint64_t)gw[wb + 1] << 32) | gw[wb]) >> (8 * (j0 & 3)));
+        uint32_t D0 = digits[bytes & 0xFFu] | (digits[(bytes >> 8) & 0xFFu] << 10) |
+                      (digits[(bytes >> 16) & 0xFFu] << 20);
+        D0 >>= 2 * d0;   // digit e of the 8 weights at bits 2e, 2e+1
+        const uint32_t w7 = gw[7];
+        const uint32_t s0 = w7 & 0xFFFFu;
+        const int sl = kRec ? rec_s[par][gl] : -1;
+        uint32_t o[4];
+        if (!kOff && sl < 0 && (s0 & 0x7FFFu) != 0 && (s0 & 0x7C00u) != 0x7C00u) {
+          // One plane, finite nonzero scale: +0 + s0*t is exactly +0 or +-s0.
+          const uint32_t S = s0 | ((s0 ^ 0x8000u) << 16);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float t0 = (float)((int)((D0 >> (2 * e)) & 3u) - 1);
-          float a = 0.0f;
-          if (has_off) a = a + mu0;
-          if (k >= 0) a = a + mu;
-          a = a + s0f * t0;
-          if (k >= 0) {
-            const float t1 = (float)((int)((D1 >> (2 * e)) & 3u) - 1);
-            a = a + s1f * t1;
+          for (int q = 0; q < 4; ++q) o[q] = __builtin_amdgcn_perm(S, S, selector[(D0 >> (4 * q)) & 15u]);
+        } else {
+          // a = +0; a += mu0; a += mu; a += s0*t0; a += s1*t1 in fp32 (each
+          // product exact), rounded once.
+          const float s0f = half_bits_to_float(s0);
+          const float mu0 = half_bits_to_float(w7 >> 16);
+          float mu = 0.0f, s1f = 0.0f;
+          uint32_t D1 = 0;
+          if (kRec && sl >= 0) {
+            const uint32_t* rw = rcd_s + 8 * sl;
+            mu = half_bits_to_float(rw[7] & 0xFFFFu);
+            s1f = half_bits_to_float(rw[7] >> 16);
+            const uint32_t rb = (uint32_t)((((uint64_t)rw[wb + 1] << 32) | rw[wb]) >> (8 * (j0 & 3)));
+            D1 = digits[rb & 0xFFu] | (digits[(rb >> 8) & 0xFFu] << 10) | (digits[(rb >> 16) & 0xFFu] << 20);
+            D1 >>= 2 * d0;
           }
-          h[e] = float_to_half_bits(a);
-        }
+          uint32_t h[8];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) o[i] = h[2 * i] | (h[2 * i + 1] << 16);
+          for (int e = 0; e < 8; ++e) {
+            const float tz = (float)((int)((D0 >> (2 * e)) & 3u) - 1);
+            float a = 0.0f;
+            if (kOff) a = a + mu0;
+            if (kRec && sl >= 0) a = a + mu;
+            a = a + s0f * tz;
+            if (kRec && sl >= 0) {
+              const float t1v = (float)((int)((D1 >> (2 * e)) & 3u) - 1);
+              a = a + s1f * t1v;
+            }
+            h[e] = float_to_half_bits(a);
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) o[q] = h[2 * q] | (h[2 * q + 1] << 16);
+        }
+        // Streaming output: nontemporal 16-byte store.
+        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+        const u32x4 ov = {o[0], o[1], o[2], o[3]};
+        __builtin_nontemporal_store(ov, reinterpret_cast<u32x4*>(w + (f0 + gl) * kGroup + p0));
       }
-      *reinterpret_cast<uint4*>(w + (f0 + g) * kGroup + p0) = make_uint4(o[0], o[1], o[2], o[3]);
+    };
+    if (kExact) {
+      pass(0);   // straight-line, so the stores are always the newest memory operations
+    } else {
+      for (int it0 = 0; it0 < n_items; it0 += kBlockItems) pass(it0);
     }
-    __syncthreads();
+  };
+
+  // Prologue: the first block in registers, the second block's row pointers
+  // in flight.  The first step is peeled so that the loop is entered only
+  // after a step's stores.
+  if (kRec) {
+    load_rowptr(b0);
+    load_records(b0);
+    clear_map(b0, 0);
+  }
+  load_plane0(b0);
+  if (kRec) load_rowptr(b0 + gs);
+  __syncthreads();
+  step(b0, 0);
+  int par = 1;
+  for (int64_t b = b0 + gs; b < n_blocks; b += gs) {
+    __syncthreads();   // the previous block's LDS reads are done
+    step(b, par);
+    par ^= 1;
   }
 }
 
@@ -568,9 +635,44 @@ hipError_t launch_validate(const uint8_t* codes, int64_t n, int32_t* d_err, hipS
 }
 
 hipError_t launch_unpack_fp16(const MatDev& m, uint16_t* w, hipStream_t s) {
-  const int64_t blocks = clamp_blocks(m.n_out, kRowMaxBlocks);
-  const size_t lds = (size_t)m.n_groups * (2 * 8 * 4 + 4 + 2 + 2);
-  hipLaunchKernelGGL(unpack_fp16_kernel, dim3((unsigned)blocks), dim3(kRowThreads), lds, s, m, w);
+  static int cus_of[64];   // CUs per device, read once
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  int& cus = cus_of[dev & 63];
+  if (cus == 0) {
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+  }
+  // An exact fit: 16 * RB * G = 256 * items with RB | N, the most items first.
+  const int G = m.n_groups;
+  int RB = 0, items = 0;
+  for (int c : {8, 6, 5}) {
+    const int rb = 16 * c / G;
+    if ((16 * c) % G == 0 && rb >= 1 && rb <= kDqMaxRows && m.n_out % rb == 0) {
+      RB = rb;
+      items = c;
+      break;
+    }
+  }
+  const bool rec = m.nnz1 > 0, off = m.offset0 != nullptr;
+  void (*kernel)(MatDev, uint16_t*, int);
+#define TQ_DQ_PICK(I, E)                                                                     \
+  (rec ? (off ? unpack_fp16_kernel<true, true, I, E> : unpack_fp16_kernel<true, false, I, E>) \
+       : (off ? unpack_fp16_kernel<false, true, I, E> : unpack_fp16_kernel<false, false, I, E>))
+  if (items == 8) {
+    kernel = TQ_DQ_PICK(8, true);
+  } else if (items == 6) {
+    kernel = TQ_DQ_PICK(6, true);
+  } else if (items == 5) {
+    kernel = TQ_DQ_PICK(5, true);
+  } else {
+    kernel = TQ_DQ_PICK(kDqGeneralItems, false);
+    RB = dq_general_rows(G);
+  }
+#undef TQ_DQ_PICK
+  const int64_t blocks = clamp_blocks(((int64_t)m.n_out + RB - 1) / RB, (int64_t)kDqBlocksPerCU * cus);
+  hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kDqThreads), 0, s, m, w, RB);
   return hipGetLastError();
 }
 
