@@ -104,13 +104,15 @@ def test_unpack_fp16_bit_exact(shape, f2):
 
 
 @pytest.mark.parametrize("shape,f2,offsets", [((8200, 4096), 0.10, False), ((8200, 4096), 0.036, True),
+                                              ((8200, 4096), 0.0, False), ((8201, 4096), 0.10, False),
                                               ((16387, 256), 0.25, False), ((1030, 32768), 0.10, False)])
 def test_unpack_fp16_more_row_blocks_than_workgroups(shape, f2, offsets):
     # More row blocks than persistent workgroups, so workgroups run several
     # pipelined steps: K = 4096 takes the exact-fit variant (4 rows of 32
-    # groups per block), K = 256 the bounds-checked one with a ragged last
-    # block (8 rows of 2 groups), K = 32768 the bounds-checked one with two
-    # passes per block.
+    # groups per block; also without records), N = 8201 rows the
+    # bounds-checked one (4 does not divide N), K = 256 the bounds-checked one
+    # with a ragged last block (8 rows of 2 groups), K = 32768 the
+    # bounds-checked one with two passes per block.
     n_out, n_in = shape
     log(f"unpack_fp16 pipelined {shape} f2={f2} offsets={offsets}")
     inp = synth.linear(n_out, n_in, f2, (31, 32, 33, n_out), offset0=offsets)
