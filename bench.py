@@ -372,6 +372,7 @@ def config_suite(dev, min_bytes=1 << 30, reps=5):
         us = graph_time_us([lambda m=m: tq.tq_gemv(m, xd, y=y, stream=torch.cuda.current_stream()) for m in mats],
                            reps=reps)
         nbytes = base.nbytes() + 2 * inp.n_in + 2 * inp.n_out
+        log(f"{label}: {us:.3f} us per call")
         lines.append({"bench": "config_cold", "config": label, "shape": f"{inp.n_out}x{inp.n_in}",
                       "two_plane_groups": inp.nnz1, "copies": n, "us_per_call": round(us, 3),
                       "bytes": nbytes, "GBps": round(nbytes / us / 1e3, 1),
@@ -394,6 +395,7 @@ def config_suite(dev, min_bytes=1 << 30, reps=5):
     b.record()
     torch.cuda.synchronize()
     t_total = a.elapsed_time(b) * 1e3
+    log(f"cfg4 tq_unpack_fp16: {t_total:.1f} us for {len(seq)} calls")
     nbytes = sum(m.nbytes() + 2 * m.n_out * m.n_in for m in seq)
     nw = sum(m.n_out * m.n_in for m in seq)
     lines.append({"bench": "config_cold", "config": "cfg4 tq_unpack_fp16, 36-layer set (252 matrices)",
@@ -546,6 +548,8 @@ def main():
                     help="also print one cold-cache line per configuration (single launches over >= 1 GiB of copies)")
     ap.add_argument("--extra", action="store_true",
                     help="also print small-batch, codec and 4096 x 2560 comparison lines")
+    ap.add_argument("--configs-only", action="store_true",
+                    help="print only the --configs lines (no decode-step line; for profiler runs)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the packed GEMV path is single-device; "
@@ -559,6 +563,11 @@ def main():
     tq.lib()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+
+    if args.configs_only:
+        for line in config_suite(dev):
+            print(json.dumps(line), flush=True)
+        return
 
     mats, xs = build_stack(args.layers, dev)
     launches = step_launches(mats, xs)
