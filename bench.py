@@ -319,6 +319,22 @@ def paper_representation_line(dev, layers=36, steps=10, warmup=3):
     return line
 
 
+def graph_node_floor(dev, nodes=144, reps=5, back_to_back=10):
+    """Per-node time of a HIP graph of `nodes` nearly empty launches
+    (tq_validate over one group: one workgroup reading 26 bytes), timed like
+    the step: the gap between graph nodes, the dispatch and one memory round
+    trip.  A stage's per-launch time minus this floor is what its work adds
+    to a launch that does almost nothing."""
+    import torch
+
+    from paper_2609_09240_amd import tq
+    codes = torch.zeros(64, dtype=torch.uint8, device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    us = graph_time_us([lambda: tq.tq_validate(codes, 1, d_err=err, stream=torch.cuda.current_stream())] * nodes,
+                       reps=reps, back_to_back=back_to_back)
+    return {"us_per_node": round(us, 3), "nodes": nodes, "kernel": "validate_kernel over one group"}
+
+
 def per_stage(mats, xs, reps=5, back_to_back=10):
     """Each stage kind of the step (q+k+v, o, gate+up, down) timed on its
     own: a HIP graph of its 36 launches (one per layer, each on that layer's
@@ -591,7 +607,11 @@ def main():
     del chain, outs_chain, graph, outs_graph
     torch.cuda.empty_cache()
     stages = per_stage(mats, xs)
-    log("per stage: " + ", ".join(f"{k} {v['us_per_launch']} us" for k, v in stages.items()))
+    node_floor = graph_node_floor(dev)
+    for v in stages.values():
+        v["us_minus_node_floor"] = round(v["us_per_launch"] - node_floor["us_per_node"], 3)
+    log("per stage: " + ", ".join(f"{k} {v['us_per_launch']} us" for k, v in stages.items())
+        + f"; graph node floor {node_floor['us_per_node']} us")
     use_chain = ms_chain <= ms_graph
     ms_per_step = ms_chain if use_chain else ms_graph
     spread = spread_chain if use_chain else spread_graph
@@ -669,6 +689,7 @@ def main():
             "avg_launch_us": round(avg_ms * 1e3, 3),
             "bytes_per_launch": round(step_bytes / nl, 1),
             "per_stage": stages,
+            "graph_node_floor": node_floor,
             "dominant": max(stages, key=lambda k: stages[k]["us_per_launch"]),
         },
     }
