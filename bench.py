@@ -441,6 +441,7 @@ def extra_suite(dev):
             Y = torch.empty(B, inp.n_out, dtype=torch.float16, device=dev)
             calls = [lambda m=m: tq.tq_gemm_smallbatch(m, X, Y=Y, stream=torch.cuda.current_stream()) for m in mats]
             us = graph_time_us(calls)
+            log(f"small batch {name} B={B}: {us:.2f} us per call")
             nbytes = base.nbytes() + 2 * B * (inp.n_in + inp.n_out)
             tflops = 2.0 * B * inp.n_out * inp.n_in / (us * 1e-6) / 1e12
             lines.append({"bench": "smallbatch", "matrix": f"{name} {inp.n_out}x{inp.n_in}", "batch": B,

@@ -15,8 +15,8 @@
 // byte 8u / 5) are fixed per step, known at compile time.
 //
 // Decode.  The GEMV's table (fp16 +-1/0 patterns (t0,t1), (t2,t3), (t4,0)
-// per code, 16 copies, static LDS) is read once per code byte (a
-// byte shared by two windows is kept in registers); a window's four dwords
+// per code, 16 copies, static LDS) is read once per code byte, with one
+// 16-byte read (a byte shared by two windows is kept in registers); a window's four dwords
 // are table dwords or two of them joined by v_alignbit / v_lshl_or.  A
 // weight is pattern * s0 + offset in one v_pk_fma_f16 (exact without
 // offsets); on two-plane groups the plane-1 pattern * s1 is added with one
@@ -124,6 +124,14 @@ __device__ __attribute__((always_inline)) inline uint32_t code_byte_addr(const u
     case 2: return q_addr<2>(word, slot);
     default: return q_addr<3>(word, slot);
   }
+}
+
+// Table entry at LDS byte address a, read whole: a 16-byte read puts the 16
+// lanes served together on 64 different banks (one copy each), where a
+// 12-byte read is split by the compiler into reads that share banks.
+__device__ __attribute__((always_inline)) inline U3 table_entry(const unsigned char* lut, uint32_t a) {
+  const u4v v = *reinterpret_cast<const u4v*>(lut + a);
+  return U3{v.x, v.y, v.z};
 }
 
 // Patterns of a window of phase o from the table entries of its bytes: the
@@ -393,9 +401,9 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
       const bool shared = u > 0 && win_last(u - 1) == j0;   // first byte already read
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
-        const U3 a0 = shared ? ep0[rt] : *reinterpret_cast<const U3*>(lut + code_byte_addr(cw[qi][rt], j0, slot));
-        const U3 a1 = *reinterpret_cast<const U3*>(lut + code_byte_addr(cw[qi][rt], j0 + 1, slot));
-        const U3 a2 = jl > j0 + 1 ? *reinterpret_cast<const U3*>(lut + code_byte_addr(cw[qi][rt], jl, slot)) : a1;
+        const U3 a0 = shared ? ep0[rt] : table_entry(lut, code_byte_addr(cw[qi][rt], j0, slot));
+        const U3 a1 = table_entry(lut, code_byte_addr(cw[qi][rt], j0 + 1, slot));
+        const U3 a2 = jl > j0 + 1 ? table_entry(lut, code_byte_addr(cw[qi][rt], jl, slot)) : a1;
         ep0[rt] = a2;
         uint32_t p[4], w[4];
         window_patterns(win_phase(u), a0, a1, a2, p);
@@ -403,9 +411,9 @@ __global__ void __launch_bounds__(kQThreads) quad_kernel(QArgs a) {
         for (int i = 0; i < 4; ++i) w[i] = hfma2(p[i], s0v[rt], c0v[rt]);
         if (hr[rt]) {
           const uint32_t* rc = kRcRegs ? rcr[rt] : rcs[rt];
-          const U3 b0 = shared ? ep1[rt] : *reinterpret_cast<const U3*>(lut + code_byte_addr(rc, j0, slot));
-          const U3 b1 = *reinterpret_cast<const U3*>(lut + code_byte_addr(rc, j0 + 1, slot));
-          const U3 b2 = jl > j0 + 1 ? *reinterpret_cast<const U3*>(lut + code_byte_addr(rc, jl, slot)) : b1;
+          const U3 b0 = shared ? ep1[rt] : table_entry(lut, code_byte_addr(rc, j0, slot));
+          const U3 b1 = table_entry(lut, code_byte_addr(rc, j0 + 1, slot));
+          const U3 b2 = jl > j0 + 1 ? table_entry(lut, code_byte_addr(rc, jl, slot)) : b1;
           ep1[rt] = b2;
           uint32_t p1[4];
           window_patterns(win_phase(u), b0, b1, b2, p1);
